@@ -1,0 +1,297 @@
+#!/usr/bin/env python3
+"""Decode-attention benchmark over the packed low-bit KV cache on one MI355X.
+
+Default workload (the headline): Llama-3.1-8B-shaped layers (32 query heads,
+8 kv heads, head dim 128), batch 1, 131072 cached tokens, K1V1 with groups of
+32, 32 layers with independent seeded caches.  One step = for every layer,
+append one token (kvq_append) then decode one token (kvq_decode_attention).
+Inputs are synthetic and resident in HBM before timing; the 32 caches
+(2 GiB) rotate through HBM, well beyond the 256 MB last-level cache.
+
+Prints ONE JSON line.  value = packed-KV bytes the decode kernels must read
+per step (codes + fp16 scales/zeros + fp16 tail, all layers) / step time.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "decode-attn effective KV GB/s (% of HBM peak) + µs/layer, K1V1 @128K ctx"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def packed_bytes(L: int, w, bk: int, bv: int) -> int:
+    """Bytes decode attention must read for one sequence of L tokens (all kv heads)."""
+    past = L - w.window
+    Lq = 0 if past <= 0 else past // w.key_group * w.key_group
+    per_tok = 16 * bk + 16 * bv + 2 * w.head_dim * 2 // w.key_group + (w.head_dim // w.value_group) * 4
+    return w.num_kv_heads * (Lq * per_tok + (L - Lq) * w.head_dim * 2 * 2)
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("decode.hip", "kvq_internal.h"):
+        with open(os.path.join(ROOT, "paper_2607_16248_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(name: str):
+    """HBM bytes per launch from a committed counter summary, if it matches the kernel source."""
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != source_digest():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, kv_heads: int):
+    """The oracle (fp64 dequantization + attention) on a bounded sample of one layer."""
+    import numpy as np
+
+    import oracle
+    from workloads import gen_kv, gen_q
+
+    heads = list(range(kv_heads))
+    L = w.lens[0]
+    bk, bv = w.bits_k[0], w.bits_v[0]
+    K, V = gen_kv(w, 0, 0, heads=heads)
+    q = gen_q(w)
+    imgs = [oracle.build_head(K[:, h], V[:, h], bk, bv, w.key_group, w.value_group, w.window) for h in heads]
+    del K, V
+    gq = w.group_q
+    t0 = time.perf_counter()
+    Kh = np.empty((kv_heads, L, w.head_dim))
+    Vh = np.empty_like(Kh)
+    for i, img in enumerate(imgs):
+        Kh[i], Vh[i] = oracle.dequant_head(img, L, w.head_dim, bk, bv, w.key_group, w.value_group, w.window)
+    oracle.attention(q[:kv_heads * gq], Kh, Vh)
+    dt = time.perf_counter() - t0
+    nbytes = packed_bytes(L, w, bk, bv) * kv_heads // w.num_kv_heads
+    threads = oracle.num_threads()
+    return {
+        "value": round(nbytes / dt / 1e9, 4),
+        "unit": "GB/s",
+        "cores": min(threads, kv_heads * gq),
+        "kind": "oracle",
+        "sample": (f"{kv_heads} of {w.num_kv_heads} kv heads ({kv_heads * gq} query heads) of one "
+                   f"{L}-token K{bk}V{bv} layer: fp64 dequantization (one thread per call) + fp64 "
+                   f"attention (OpenMP over query heads, {min(threads, kv_heads * gq)} threads); "
+                   f"{dt:.2f} s for {nbytes / 1e6:.1f} MB of packed KV; "
+                   f"{dt * 1e6 * w.num_kv_heads / kv_heads:.0f} us per full layer"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, help="0-4; 2 is the headline")
+    ap.add_argument("--bits", type=int, default=None, help="bit width for workload 4")
+    ap.add_argument("--kernel-iters", type=int, default=256)
+    ap.add_argument("--cpu-heads", type=int, default=4, help="kv heads in the CPU-baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is not "
+              f"part of this library", file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_16248_amd import kvq
+    from workloads import gen_append, gen_kv_device, gen_q, workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = workload(args.workload, args.bits)
+    steps, warm = args.steps, args.warmup
+    appending = args.workload == 2
+    per_layer = max(packed_bytes(L, w, bk, bv) for L, bk, bv in zip(w.lens, w.bits_k, w.bits_v))
+    layers = w.layers if w.layers > 1 else max(1, min(64, -(-(1 << 30) // max(1, sum(
+        packed_bytes(L, w, bk, bv) for L, bk, bv in zip(w.lens, w.bits_k, w.bits_v))))))
+    extra = (steps + warm + 2) if appending else 0
+    cap = max(w.lens) + extra
+
+    log(f"[bench] workload {w.name}: {layers} layer caches, capacity {cap}")
+    caches, qs, outs = [], [], []
+    for l in range(layers):
+        c = kvq.KVCache(w.batch, w.num_q_heads, w.num_kv_heads, cap, list(w.bits_k), list(w.bits_v),
+                        key_group=w.key_group, value_group=w.value_group, fp16_window=w.window, device=dev)
+        nmax = max(w.lens)
+        Kb = torch.zeros((w.batch, nmax, w.num_kv_heads, w.head_dim), dtype=torch.float16, device=dev)
+        Vb = torch.zeros_like(Kb)
+        for s in range(w.batch):
+            K, V = gen_kv_device(w, l, s, w.lens[s], dev, torch)
+            Kb[s, :w.lens[s]] = K
+            Vb[s, :w.lens[s]] = V
+            del K, V
+        c.append(Kb, Vb, list(w.lens))
+        del Kb, Vb
+        import numpy as np
+        qs.append(torch.from_numpy(np.stack([gen_q(w, l, s) for s in range(w.batch)])).to(dev))
+        outs.append(torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev))
+        caches.append(c)
+    torch.cuda.synchronize()
+    for c in caches:
+        c.check()
+    ws_bytes = max(kvq.kvq_workspace_bytes(c.handle) for c in caches)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+
+    # appended tokens for every step, generated up front and resident on the device
+    app = []
+    if appending:
+        for st in range(steps + warm + 1):
+            row = []
+            for l in range(layers):
+                Kn, Vn = gen_append(w, l, 0, st)
+                row.append((torch.from_numpy(Kn[None]).to(dev), torch.from_numpy(Vn[None]).to(dev)))
+            app.append(row)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream().cuda_stream
+    one = [1] * w.batch
+    handles = [c.handle for c in caches]
+
+    def step(st):
+        for l in range(layers):
+            if appending:
+                kvq.kvq_append(handles[l], app[st][l][0], app[st][l][1], one, n_max=1, stream=stream)
+            kvq.kvq_decode_attention(handles[l], qs[l], outs[l], ws, ws_bytes, stream=stream)
+
+    log(f"[bench] warmup {warm} steps")
+    for st in range(warm):
+        step(st)
+    torch.cuda.synchronize()
+
+    lens_before = [[kvq.kvq_seq_len(h, s) for s in range(w.batch)] for h in handles]
+    moved = 0
+    for st in range(steps):
+        for l in range(layers):
+            for s in range(w.batch):
+                L = lens_before[l][s] + ((st + 1) if appending else 0)
+                moved += packed_bytes(L, w, w.bits_k[s], w.bits_v[s])
+
+    log(f"[bench] timing {steps} steps")
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record()
+    for st in range(steps):
+        step(warm + st)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = ev0.elapsed_time(ev1) / steps
+    for c in caches:
+        c.check()
+
+    # dominant kernel alone: split kernels of kvq_decode_partials, back to back
+    # over the rotating layer caches, timed with events on the launch stream
+    def timed(fn, iters):
+        for i in range(8):
+            fn(i)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(iters):
+            fn(i)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / iters  # microseconds
+
+    it = args.kernel_iters
+    split_us = timed(lambda i: kvq.kvq_decode_partials(handles[i % layers], qs[i % layers], ws, ws_bytes,
+                                                       stream=stream), it)
+    merge_us = timed(lambda i: kvq.kvq_decode_merge(handles[i % layers], ws, outs[i % layers], stream=stream), it)
+    decode_us = timed(lambda i: kvq.kvq_decode_attention(handles[i % layers], qs[i % layers], outs[i % layers],
+                                                         ws, ws_bytes, stream=stream), it)
+    L_now = [kvq.kvq_seq_len(handles[0], s) for s in range(w.batch)]
+    launch_bytes = sum(packed_bytes(L, w, bk, bv) for L, bk, bv in zip(L_now, w.bits_k, w.bits_v))
+    achieved = launch_bytes / (split_us * 1e-6) / 1e9
+
+    value = moved / (step_ms * 1e-3) / 1e9
+    us_per_layer = step_ms * 1e3 / layers
+    traffic_name = f"decode_split_{w.name}_traffic.txt"
+    traffic = read_traffic(traffic_name)
+
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32 (1-bit codes, fp16 scales)" if w.bits_k[0] == 1 else "fp32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "layers": layers,
+            "batch": w.batch,
+            "num_q_heads": w.num_q_heads,
+            "num_kv_heads": w.num_kv_heads,
+            "head_dim": w.head_dim,
+            "context": list(w.lens) if w.batch <= 4 else f"{min(w.lens)}..{max(w.lens)}",
+            "bits": [f"K{a}V{b}" for a, b in sorted(set(zip(w.bits_k, w.bits_v)))],
+            "key_group": w.key_group,
+            "value_group": w.value_group,
+            "fp16_window": w.window,
+            "append_per_step": appending,
+            "parallelism": "single GPU, split-K over tokens",
+        },
+        "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "us_per_layer": round(us_per_layer, 3),
+        "decode_us_per_layer": round(decode_us, 3),
+        "split_kernel_us": round(split_us, 3),
+        "merge_kernel_us": round(merge_us, 3),
+        "bytes_per_layer": launch_bytes,
+        "wall_s_timed": round(wall, 4),
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "kernel": f"decode_split_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.group_q}>",
+            "bytes_per_launch": launch_bytes,
+            "kernel_source_sha256_16": source_digest(),
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] CPU baseline (oracle)")
+        result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_heads, w.num_kv_heads))
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

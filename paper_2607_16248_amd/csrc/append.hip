@@ -1,0 +1,174 @@
+// Quantize-on-append for the packed low-bit KV cache (gfx950).
+//
+// One launch packs every key group that leaves the fp16 window and copies
+// the remaining new tokens into the per-head fp16 ring.  The quantizer is
+// asymmetric min-max with an fp16 scale rounded up and an fp16 zero-point
+// equal to the group minimum; codes round half to even.  The paper names
+// b-bit keys and values (Motivation, "Accuracy Loss under Aggressive KV
+// Quantization") and asymmetric key/value formats (Related Work) but leaves
+// the rule open; this is the rule the library defines in kvq.h.
+//
+// Exactness: x - z is exact in fp64, the fp64 quotient is correctly rounded
+// (IEEE divide; this file is built with -ffp-contract=off and no fast-math)
+// and rint() rounds half to even, so codes equal the exact rational
+// round-half-even.  Off the decode hot path: a key group flushes once every
+// key_group appended tokens.
+#include <hip/hip_runtime.h>
+
+#include "kvq_internal.h"
+
+namespace kvq {
+namespace {
+
+__device__ __forceinline__ double half_bits_to_double(uint16_t h) {
+  return (double)__builtin_bit_cast(_Float16, h);
+}
+
+// Smallest fp16 (bit pattern) whose value is >= s, for 0 <= s <= 65504.
+// Start from a rounded conversion and walk to the exact answer: positive fp16
+// patterns increase with their value, and the conversion is within an ulp.
+__device__ __forceinline__ bool half_ceil(double s, uint16_t& out) {
+  if (!(s <= 65504.0) || !(s >= 0.0)) return false;
+  if (s == 0.0) { out = 0; return true; }
+  uint16_t b = __builtin_bit_cast(uint16_t, (_Float16)(float)s);
+  while (half_bits_to_double(b) < s) ++b;
+  while (b > 1 && half_bits_to_double((uint16_t)(b - 1)) >= s) --b;
+  out = b;
+  return true;
+}
+
+__device__ __forceinline__ void raise_range(uint8_t* arena) {
+  *reinterpret_cast<volatile uint32_t*>(arena) = 4u;  // KVQ_ERR_RANGE
+}
+
+__device__ __forceinline__ const uint16_t* token_row(const AppendArgs& a, const AppendSeq& S,
+                                                     const uint8_t* blk, uint32_t ring,
+                                                     const uint16_t* in, int h, int p) {
+  if (p < S.L_old) return reinterpret_cast<const uint16_t*>(blk + ring) + (size_t)(p % a.W) * kHeadDim;
+  return in + (((size_t)S.seq * a.n_max + (p - S.L_old)) * a.hkv + h) * kHeadDim;
+}
+
+// Pack `rows` rows of 128 codes (LDS, row-major) at `bits` bits into dwords.
+__device__ __forceinline__ void pack_rows(const uint8_t* codes, int rows, int bits, uint8_t* dst) {
+  const int dw_per_row = 4 * bits, per_dw = 32 / bits;
+  for (int k = threadIdx.x; k < rows * dw_per_row; k += blockDim.x) {
+    const int i = k / dw_per_row, w = k % dw_per_row;
+    uint32_t v = 0;
+    for (int e = 0; e < per_dw; ++e) v |= (uint32_t)codes[i * kHeadDim + w * per_dw + e] << (e * bits);
+    reinterpret_cast<uint32_t*>(dst + (size_t)i * 16 * bits)[w] = v;
+  }
+}
+
+__device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, int gi, int bk,
+                               int bv, uint8_t* codes) {
+  uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;
+  const int gk = a.gk, j = S.Lq_old / gk + gi, p0 = j * gk;
+  const int c = threadIdx.x;
+
+  // keys: thread c owns channel c of the group's gk tokens
+  {
+    double mn = __builtin_inf(), mx = -__builtin_inf();
+    bool finite = true;
+    for (int i = 0; i < gk; ++i) {
+      const double v = half_bits_to_double(token_row(a, S, blk, a.tk, a.K, h, p0 + i)[c]);
+      finite &= __builtin_isfinite(v);
+      mn = v < mn ? v : mn;
+      mx = v > mx ? v : mx;
+    }
+    if (mn == 0.0) mn = 0.0;  // +0 zero-point
+    uint16_t sb = 0;
+    const bool ok = finite && half_ceil((mx - mn) / (double)((1 << bk) - 1), sb);
+    if (!ok) { raise_range(a.arena); sb = 0x7E00; }
+    const double sv = half_bits_to_double(sb);
+    for (int i = 0; i < gk; ++i) {
+      const double v = half_bits_to_double(token_row(a, S, blk, a.tk, a.K, h, p0 + i)[c]);
+      codes[i * kHeadDim + c] = (ok && sv != 0.0) ? (uint8_t)__builtin_rint((v - mn) / sv) : 0;
+    }
+    uint16_t* km = reinterpret_cast<uint16_t*>(blk + a.km) + (size_t)j * 2 * kHeadDim;
+    km[c] = sb;
+    km[kHeadDim + c] = __builtin_bit_cast(uint16_t, (_Float16)mn);
+  }
+  __syncthreads();
+  pack_rows(codes, gk, bk, blk + a.kc + (size_t)p0 * 16 * bk);
+  __syncthreads();
+
+  // values: one item per (token, value group)
+  const int ng = kHeadDim / a.gv;
+  for (int it = threadIdx.x; it < gk * ng; it += blockDim.x) {
+    const int i = it / ng, g = it % ng;
+    const uint16_t* row = token_row(a, S, blk, a.tv, a.V, h, p0 + i) + g * a.gv;
+    double mn = __builtin_inf(), mx = -__builtin_inf();
+    bool finite = true;
+    for (int e = 0; e < a.gv; ++e) {
+      const double v = half_bits_to_double(row[e]);
+      finite &= __builtin_isfinite(v);
+      mn = v < mn ? v : mn;
+      mx = v > mx ? v : mx;
+    }
+    if (mn == 0.0) mn = 0.0;
+    uint16_t sb = 0;
+    const bool ok = finite && half_ceil((mx - mn) / (double)((1 << bv) - 1), sb);
+    if (!ok) { raise_range(a.arena); sb = 0x7E00; }
+    const double sv = half_bits_to_double(sb);
+    for (int e = 0; e < a.gv; ++e) {
+      const double v = half_bits_to_double(row[e]);
+      codes[i * kHeadDim + g * a.gv + e] = (ok && sv != 0.0) ? (uint8_t)__builtin_rint((v - mn) / sv) : 0;
+    }
+    const uint32_t zb = __builtin_bit_cast(uint16_t, (_Float16)mn);
+    reinterpret_cast<uint32_t*>(blk + a.vm)[(size_t)(p0 + i) * ng + g] = (uint32_t)sb | (zb << 16);
+  }
+  __syncthreads();
+  pack_rows(codes, gk, bv, blk + a.vc + (size_t)p0 * 16 * bv);
+}
+
+// Copy the new tokens that stay fp16 into the ring of head h.
+__device__ void copy_ring(const AppendArgs& a, const AppendSeq& S, int h) {
+  uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;
+  uint16_t* rk = reinterpret_cast<uint16_t*>(blk + a.tk);
+  uint16_t* rv = reinterpret_cast<uint16_t*>(blk + a.tv);
+  const int first = S.Lq_new > S.L_old ? S.Lq_new : S.L_old;
+  const int c = threadIdx.x;
+  for (int p = first; p < S.L_new; ++p) {
+    const size_t src = (((size_t)S.seq * a.n_max + (p - S.L_old)) * a.hkv + h) * kHeadDim + c;
+    rk[(size_t)(p % a.W) * kHeadDim + c] = a.K[src];
+    rv[(size_t)(p % a.W) * kHeadDim + c] = a.V[src];
+  }
+}
+
+__global__ __launch_bounds__(128) void append_kernel(AppendArgs a, int bk, int bv) {
+  __shared__ uint8_t codes[128 * kHeadDim];
+  const int wg = blockIdx.x;
+  int si = 0;
+  for (int i = 1; i < a.nseq; ++i) si = (a.seq[i].wg_begin <= wg) ? i : si;
+  const AppendSeq& S = a.seq[si];
+  const int local = wg - S.wg_begin;
+  const int nquant = a.quantize ? S.n_quant * a.hkv : 0;
+  if (local < nquant) {
+    quantize_group(a, S, local / S.n_quant, local % S.n_quant, bk, bv, codes);
+  } else if (S.do_copy) {
+    copy_ring(a, S, local - nquant);
+  }
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
+}  // namespace
+
+int launch_append(const AppendArgs& a, int bk, int bv, void* stream) {
+  if (a.total_wg <= 0) return 0;
+  hipLaunchKernelGGL(append_kernel, dim3(a.total_wg), dim3(128), 0, (hipStream_t)stream, a, bk, bv);
+  return (int)hipGetLastError();
+}
+
+int launch_fill_zero(void* dst, size_t words, void* stream) {
+  if (words == 0) return 0;
+  const unsigned blocks = (unsigned)((words + 255) / 256 < 1024 ? (words + 255) / 256 : 1024);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                     (uint32_t*)dst, words);
+  return (int)hipGetLastError();
+}
+
+}  // namespace kvq

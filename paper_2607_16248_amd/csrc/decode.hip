@@ -1,0 +1,414 @@
+// Single-token decode attention over the packed low-bit KV cache (gfx950).
+//
+// out = softmax(q K^T / sqrt(d)) V for every query head (Introduction: the
+// scaled dot-product attention the decoder runs at each step), with K and V
+// dequantized in registers straight from the packed codes.
+//
+// Split-K over tokens (flash-decoding): each workgroup owns one
+// (sequence, kv head, token range) and keeps an online softmax in base 2 for
+// the Hq/Hkv query heads that read that kv head; a merge pass combines the
+// per-split (max, sum, accumulator) records.  The packed codes carry no
+// matrix-core-sized work (each token is a rank-GQ matrix-vector product), so
+// everything runs on the vector ALUs:
+//   - key scales are folded into the query once per key group,
+//       q'_c = q_c * s_c * log2(e)/sqrt(d),   bias = sum_c q_c * z_c * log2(e)/sqrt(d),
+//     so a score is bias + sum_c q'_c * code_c;
+//   - values are dequantized per element as fma(code, s, z) and accumulated;
+//   - wave-wide max and sum use DPP row operations and the row broadcasts.
+#include <hip/hip_runtime.h>
+
+#include "kvq_internal.h"
+
+namespace kvq {
+namespace {
+
+constexpr int kWaves = 4;
+
+__device__ __forceinline__ float h2f(uint32_t bits16) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
+}
+
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_mov(float old, float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
+                                                               __builtin_bit_cast(int, v), CTRL,
+                                                               ROW_MASK, 0xF, false));
+}
+
+// DPP controls: quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror,
+// row_mirror, row_bcast:15, row_bcast:31.
+constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kHalfMirror = 0x141, kMirror = 0x140,
+              kBcast15 = 0x142, kBcast31 = 0x143;
+
+__device__ __forceinline__ float readlane63(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_mov<kQuadXor1>(0.f, v);
+  v += dpp_mov<kQuadXor2>(0.f, v);
+  v += dpp_mov<kHalfMirror>(0.f, v);
+  v += dpp_mov<kMirror>(0.f, v);
+  v += dpp_mov<kBcast15, 0xA>(0.f, v);
+  v += dpp_mov<kBcast31, 0xC>(0.f, v);
+  return readlane63(v);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  const float ninf = -__builtin_inff();
+  v = fmaxf(v, dpp_mov<kQuadXor1>(ninf, v));
+  v = fmaxf(v, dpp_mov<kQuadXor2>(ninf, v));
+  v = fmaxf(v, dpp_mov<kHalfMirror>(ninf, v));
+  v = fmaxf(v, dpp_mov<kMirror>(ninf, v));
+  v = fmaxf(v, dpp_mov<kBcast15, 0xA>(ninf, v));
+  v = fmaxf(v, dpp_mov<kBcast31, 0xC>(ninf, v));
+  return readlane63(v);
+}
+
+// LDS written and read back by the same wave: order the accesses.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Key row half (64 channels): 8*B bytes = 2*B dwords.
+template <int B>
+__device__ __forceinline__ void load_key_half(const uint8_t* row, uint32_t (&w)[2 * B]) {
+  if constexpr (B == 1) {
+    const uint2 v = *reinterpret_cast<const uint2*>(row);
+    w[0] = v.x; w[1] = v.y;
+  } else {
+#pragma unroll
+    for (int i = 0; i < B / 2; ++i) {
+      const uint4 v = reinterpret_cast<const uint4*>(row)[i];
+      w[4 * i] = v.x; w[4 * i + 1] = v.y; w[4 * i + 2] = v.z; w[4 * i + 3] = v.w;
+    }
+  }
+}
+
+// Value bits of 8 consecutive channels (8*B bits) of one token row.
+template <int B>
+__device__ __forceinline__ uint64_t load_value8(const uint8_t* row, int cc) {
+  if constexpr (B == 1) return row[cc];
+  else if constexpr (B == 2) return reinterpret_cast<const uint16_t*>(row)[cc];
+  else if constexpr (B == 4) return reinterpret_cast<const uint32_t*>(row)[cc];
+  else return reinterpret_cast<const uint64_t*>(row)[cc];
+}
+
+template <int GQ>
+struct QStride {
+  static constexpr int value = GQ <= 4 ? GQ : 8;
+};
+
+template <int GQ>
+struct State {
+  float m[GQ];
+  float l[GQ];
+  float acc[GQ][8];
+};
+
+// Online-softmax update for one pass of 32 tokens held as sig (QK layout:
+// lanes 2t, 2t+1 hold token t).  Writes p to LDS, rescales the state.
+template <int GQ>
+__device__ __forceinline__ void softmax_pass(State<GQ>& st, float (&sig)[GQ], int half, int tl,
+                                             float* p_lds) {
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) {
+    const float mx = wave_max(sig[g]);
+    const float mnew = fmaxf(st.m[g], mx);
+    const float alpha = __builtin_amdgcn_exp2f(st.m[g] - mnew);
+    const float p = __builtin_amdgcn_exp2f(sig[g] - mnew);
+    st.l[g] = st.l[g] * alpha + (half ? 0.f : p);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) st.acc[g][k] *= alpha;
+    st.m[g] = mnew;
+    if (!half) p_lds[tl * GQ + g] = p;
+  }
+}
+
+template <int BK, int BV, int GQ>
+__device__ __forceinline__ void packed_group(const DecodeArgs& a, const uint8_t* blk, int j,
+                                             const float (&qs0)[GQ], const float (&qs1)[GQ],
+                                             float* qp, float* p_lds, State<GQ>& st, int lane) {
+  constexpr int QS = QStride<GQ>::value;
+  // scales and zeros of the key group: this lane's channels 2*lane, 2*lane+1
+  const uint32_t* km = reinterpret_cast<const uint32_t*>(blk + a.km + (size_t)j * 2 * kHeadDim * 2);
+  const uint32_t sw = km[lane], zw = km[kHeadDim / 2 + lane];
+  const float s0 = h2f(sw & 0xFFFF), s1 = h2f(sw >> 16), z0 = h2f(zw & 0xFFFF), z1 = h2f(zw >> 16);
+  float bias[GQ];
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) {
+    qp[(2 * lane) * QS + g] = qs0[g] * s0;
+    qp[(2 * lane + 1) * QS + g] = qs1[g] * s1;
+    bias[g] = fmaf(qs0[g], z0, qs1[g] * z1);
+  }
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) bias[g] = wave_sum(bias[g]);
+  wave_lds_sync();
+
+  const int tl = lane >> 1, half = lane & 1;
+  const int tq = lane >> 4, cc = lane & 15;
+  const int ng = kHeadDim / a.gv, vg = (cc * 8) / a.gv;
+  for (int pass = 0; pass < a.gk / 32; ++pass) {
+    const int tbase = j * a.gk + pass * 32;
+    // scores: lane pair (2t, 2t+1) splits token t's 128 channels in halves
+    uint32_t kw[2 * BK];
+    load_key_half<BK>(blk + a.kc + (size_t)(tbase + tl) * 16 * BK + half * 8 * BK, kw);
+    float sig[GQ];
+#pragma unroll
+    for (int g = 0; g < GQ; ++g) sig[g] = 0.f;
+    constexpr int PER = 32 / BK;
+    constexpr uint32_t MASK = (1u << BK) - 1u;
+#pragma unroll
+    for (int w = 0; w < 2 * BK; ++w) {
+#pragma unroll
+      for (int e = 0; e < PER; ++e) {
+        const float code = (float)((kw[w] >> (e * BK)) & MASK);
+        const float* qv = qp + (half * 64 + w * PER + e) * QS;
+#pragma unroll
+        for (int g = 0; g < GQ; ++g) sig[g] = fmaf(qv[g], code, sig[g]);
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < GQ; ++g) sig[g] += dpp_mov<kQuadXor1>(0.f, sig[g]) + bias[g];
+    softmax_pass<GQ>(st, sig, half, tl, p_lds);
+    wave_lds_sync();
+
+    // values: lane (tq, cc) owns channels 8cc..8cc+7 for tokens tq, tq+4, ...
+#pragma unroll 2
+    for (int tt = tq; tt < 32; tt += 4) {
+      const int t = tbase + tt;
+      const uint32_t meta = reinterpret_cast<const uint32_t*>(blk + a.vm)[(size_t)t * ng + vg];
+      const float sv = h2f(meta & 0xFFFF), zv = h2f(meta >> 16);
+      const uint64_t vb = load_value8<BV>(blk + a.vc + (size_t)t * 16 * BV, cc);
+      const float* pp = p_lds + tt * GQ;
+      float pg[GQ];
+#pragma unroll
+      for (int g = 0; g < GQ; ++g) pg[g] = pp[g];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float v = fmaf((float)((uint32_t)(vb >> (k * BV)) & ((1u << BV) - 1u)), sv, zv);
+#pragma unroll
+        for (int g = 0; g < GQ; ++g) st.acc[g][k] = fmaf(pg[g], v, st.acc[g][k]);
+      }
+    }
+    wave_lds_sync();
+  }
+}
+
+// fp16 tail tokens [Lq, L), read from the ring; pass `pass` covers 32 tokens.
+template <int GQ>
+__device__ __forceinline__ void tail_pass(const DecodeArgs& a, const DecodeSeq& S, const uint8_t* blk,
+                                          int pass, const float* qp, float* p_lds, State<GQ>& st,
+                                          int lane) {
+  constexpr int QS = QStride<GQ>::value;
+  const int ntail = S.L - S.Lq;
+  const int tl = lane >> 1, half = lane & 1;
+  const int idx = pass * 32 + tl;
+  float sig[GQ];
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) sig[g] = 0.f;
+  if (idx < ntail) {
+    const int slot = (S.Lq + idx) % a.W;
+    const uint4* kr = reinterpret_cast<const uint4*>(blk + a.tk + ((size_t)slot * kHeadDim + half * 64) * 2);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint4 v = kr[i];
+      const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = h2f((w4[e >> 1] >> ((e & 1) * 16)) & 0xFFFF);
+        const float* qv = qp + (half * 64 + i * 8 + e) * QS;
+#pragma unroll
+        for (int g = 0; g < GQ; ++g) sig[g] = fmaf(qv[g], x, sig[g]);
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) {
+    sig[g] += dpp_mov<kQuadXor1>(0.f, sig[g]);
+    if (idx >= ntail) sig[g] = -__builtin_inff();
+  }
+  softmax_pass<GQ>(st, sig, half, tl, p_lds);
+  wave_lds_sync();
+  const int tq = lane >> 4, cc = lane & 15;
+  for (int tt = tq; tt < 32; tt += 4) {
+    const int i2 = pass * 32 + tt;
+    if (i2 >= ntail) break;
+    const int slot = (S.Lq + i2) % a.W;
+    const uint4 v = *reinterpret_cast<const uint4*>(blk + a.tv + ((size_t)slot * kHeadDim + cc * 8) * 2);
+    const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+    const float* pp = p_lds + tt * GQ;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float x = h2f((w4[k >> 1] >> ((k & 1) * 16)) & 0xFFFF);
+#pragma unroll
+      for (int g = 0; g < GQ; ++g) st.acc[g][k] = fmaf(pp[g], x, st.acc[g][k]);
+    }
+  }
+  wave_lds_sync();
+}
+
+template <int BK, int BV, int GQ>
+__global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
+  constexpr int QS = QStride<GQ>::value;
+  __shared__ float qp_lds[kWaves][kHeadDim * QS];
+  __shared__ float p_lds[kWaves][32 * GQ];
+  __shared__ float red_m[kWaves][GQ], red_l[kWaves][GQ];
+  __shared__ float red_acc[kWaves][GQ * kHeadDim];
+
+  const int wg = blockIdx.x;
+  int si = 0;
+  for (int i = 1; i < a.nseq; ++i) si = (a.seq[i].wg_begin <= wg) ? i : si;
+  const DecodeSeq& S = a.seq[si];
+  const int local = wg - S.wg_begin;
+  const int h = local / S.nsplit, sp = local % S.nsplit;
+  const uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+
+  // this lane's two channels of the GQ query heads, pre-scaled to base 2
+  const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)h * GQ) * kHeadDim;
+  float qs0[GQ], qs1[GQ];
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) {
+    const uint32_t w = reinterpret_cast<const uint32_t*>(qrow + g * kHeadDim)[lane];
+    qs0[g] = h2f(w & 0xFFFF) * a.qscale;
+    qs1[g] = h2f(w >> 16) * a.qscale;
+  }
+
+  State<GQ> st;
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) {
+    st.m[g] = -__builtin_inff();
+    st.l[g] = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) st.acc[g][k] = 0.f;
+  }
+
+  float* qp = qp_lds[wv];
+  float* pl = p_lds[wv];
+  if (sp < S.nq) {
+    const int t0 = sp * a.split_tokens;
+    const int t1 = min(S.Lq, t0 + a.split_tokens);
+    for (int j = t0 / a.gk + wv; j < t1 / a.gk; j += kWaves)
+      packed_group<BK, BV, GQ>(a, blk, j, qs0, qs1, qp, pl, st, lane);
+  } else {
+#pragma unroll
+    for (int g = 0; g < GQ; ++g) {
+      qp[(2 * lane) * QS + g] = qs0[g];
+      qp[(2 * lane + 1) * QS + g] = qs1[g];
+    }
+    wave_lds_sync();
+    for (int pass = wv; pass * 32 < S.L - S.Lq; pass += kWaves) tail_pass<GQ>(a, S, blk, pass, qp, pl, st, lane);
+  }
+
+  // combine: lanes of a wave, then the waves of the workgroup
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) {
+    st.l[g] = wave_sum(st.l[g]);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      st.acc[g][k] += __shfl_xor(st.acc[g][k], 16);
+      st.acc[g][k] += __shfl_xor(st.acc[g][k], 32);
+    }
+  }
+  if (lane < 16) {
+#pragma unroll
+    for (int g = 0; g < GQ; ++g)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) red_acc[wv][g * kHeadDim + lane * 8 + k] = st.acc[g][k];
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int g = 0; g < GQ; ++g) { red_m[wv][g] = st.m[g]; red_l[wv][g] = st.l[g]; }
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < GQ * kHeadDim; idx += blockDim.x) {
+    const int g = idx / kHeadDim, c = idx % kHeadDim;
+    float M = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red_m[w][g]);
+    float val = 0.f, lsum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float f = __builtin_amdgcn_exp2f(red_m[w][g] - M);
+      val = fmaf(f, red_acc[w][idx], val);
+      lsum = fmaf(f, red_l[w][g], lsum);
+    }
+    float* rec = a.ws + ((size_t)(S.ws_base + sp) * a.hq + (size_t)h * GQ + g) * kRecFloats;
+    rec[4 + c] = val;
+    if (c == 0) { rec[0] = M; rec[1] = lsum; }
+  }
+}
+
+__global__ __launch_bounds__(128) void merge_kernel(MergeArgs a) {
+  const int si = blockIdx.x / a.hq, hq = blockIdx.x % a.hq;
+  const MergeSeq& S = a.seq[si];
+  const int c = threadIdx.x;
+  float* o = a.out + ((size_t)S.seq * a.hq + hq) * kHeadDim;
+  if (S.nsplit == 0) { o[c] = 0.f; return; }
+  const float* base = a.ws + ((size_t)S.ws_base * a.hq + hq) * kRecFloats;
+  const size_t step = (size_t)a.hq * kRecFloats;
+  float M = -__builtin_inff();
+  for (int i = 0; i < S.nsplit; ++i) M = fmaxf(M, base[i * step]);
+  float num = 0.f, den = 0.f;
+  for (int i = 0; i < S.nsplit; ++i) {
+    const float* rec = base + i * step;
+    const float f = __builtin_amdgcn_exp2f(rec[0] - M);
+    num = fmaf(f, rec[4 + c], num);
+    den = fmaf(f, rec[1], den);
+  }
+  o[c] = num / den;
+}
+
+template <int BK, int BV, int GQ>
+int launch_t(const DecodeArgs& a, void* stream) {
+  hipLaunchKernelGGL((decode_split_kernel<BK, BV, GQ>), dim3(a.total_wg), dim3(64 * kWaves), 0,
+                     (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+template <int BK, int BV>
+int launch_gq(const DecodeArgs& a, int gq, void* stream) {
+  switch (gq) {
+    case 1: return launch_t<BK, BV, 1>(a, stream);
+    case 2: return launch_t<BK, BV, 2>(a, stream);
+    case 4: return launch_t<BK, BV, 4>(a, stream);
+    case 5: return launch_t<BK, BV, 5>(a, stream);
+    case 8: return launch_t<BK, BV, 8>(a, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+template <int BK>
+int launch_bv(const DecodeArgs& a, int bv, int gq, void* stream) {
+  switch (bv) {
+    case 1: return launch_gq<BK, 1>(a, gq, stream);
+    case 2: return launch_gq<BK, 2>(a, gq, stream);
+    case 4: return launch_gq<BK, 4>(a, gq, stream);
+    case 8: return launch_gq<BK, 8>(a, gq, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream) {
+  if (a.total_wg <= 0) return 0;
+  switch (bk) {
+    case 1: return launch_bv<1>(a, bv, gq, stream);
+    case 2: return launch_bv<2>(a, bv, gq, stream);
+    case 4: return launch_bv<4>(a, bv, gq, stream);
+    case 8: return launch_bv<8>(a, bv, gq, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+int launch_merge(const MergeArgs& a, void* stream) {
+  if (a.nseq <= 0) return 0;
+  hipLaunchKernelGGL(merge_kernel, dim3(a.nseq * a.hq), dim3(kHeadDim), 0, (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+}  // namespace kvq

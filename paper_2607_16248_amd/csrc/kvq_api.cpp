@@ -1,0 +1,489 @@
+// C ABI of the packed low-bit KV-cache library: argument checks, host-side
+// length bookkeeping, the split plan of the decode kernel, and launches.
+//
+// Everything before a launch is plain host code that touches no device and
+// calls no HIP function, so argument and capacity errors are detected (and
+// testable) without a GPU and leave the cache unchanged.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "kvq.h"
+#include "kvq_internal.h"
+
+using kvq::HeadLayout;
+
+struct kvq_cache {
+  kvq_cache_desc d{};
+  std::vector<uint8_t> bk, bv;
+  uint8_t* arena = nullptr;
+  size_t arena_bytes = 0;
+  int64_t cq = 0;   // most tokens ever packed per sequence
+  int32_t W = 0;    // ring slots per head
+  std::vector<uint64_t> head0;
+  std::vector<HeadLayout> lay;
+  std::vector<int32_t> L, Lq;
+  int32_t split_tokens = 0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+constexpr int kMaxSplits = 512;          // packed splits per sequence and kv head
+constexpr int kMinGroupsPerSplit = 4;    // one key group per wave at least
+constexpr int kTargetWorkgroups = 2048;  // about 8 per compute unit
+
+kvq_status fail(kvq_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+kvq_status ok() {
+  g_err.clear();
+  return KVQ_OK;
+}
+
+bool valid_bits(int b) { return b == 1 || b == 2 || b == 4 || b == 8; }
+
+kvq_status check_desc(const kvq_cache_desc* d) {
+  if (!d) return fail(KVQ_ERR_ARG, "descriptor is NULL");
+  if (d->batch < 1) return fail(KVQ_ERR_ARG, "batch must be >= 1 (got %d)", d->batch);
+  if (d->num_kv_heads < 1) return fail(KVQ_ERR_ARG, "num_kv_heads must be >= 1");
+  if (d->num_q_heads < 1 || d->num_q_heads % d->num_kv_heads != 0)
+    return fail(KVQ_ERR_ARG, "num_q_heads (%d) must be a positive multiple of num_kv_heads (%d)",
+                d->num_q_heads, d->num_kv_heads);
+  const int gq = d->num_q_heads / d->num_kv_heads;
+  if (!(gq == 1 || gq == 2 || gq == 4 || gq == 5 || gq == 8))
+    return fail(KVQ_ERR_UNSUPPORTED, "num_q_heads / num_kv_heads = %d; supported: 1, 2, 4, 5, 8", gq);
+  if (d->head_dim < 1) return fail(KVQ_ERR_ARG, "head_dim must be positive");
+  if (d->head_dim != kvq::kHeadDim) return fail(KVQ_ERR_UNSUPPORTED, "head_dim %d; only 128 is supported", d->head_dim);
+  if (d->max_tokens < 1) return fail(KVQ_ERR_ARG, "max_tokens must be >= 1");
+  if (!(d->key_group == 32 || d->key_group == 64 || d->key_group == 128))
+    return fail(KVQ_ERR_ARG, "key_group %d; must be 32, 64 or 128", d->key_group);
+  const int gv = d->value_group;
+  if (!(gv == 8 || gv == 16 || gv == 32 || gv == 64 || gv == 128))
+    return fail(KVQ_ERR_ARG, "value_group %d; must be 8, 16, 32, 64 or 128", gv);
+  if (d->fp16_window < 0) return fail(KVQ_ERR_ARG, "fp16_window must be >= 0");
+  if ((int64_t)d->fp16_window + d->key_group > (int64_t)1 << 30) return fail(KVQ_ERR_ARG, "fp16_window too large");
+  if (!d->bits_k || !d->bits_v) return fail(KVQ_ERR_ARG, "bits_k and bits_v must be host arrays of length batch");
+  for (int i = 0; i < d->batch; ++i) {
+    if (!valid_bits(d->bits_k[i]) || !valid_bits(d->bits_v[i]))
+      return fail(KVQ_ERR_ARG, "sequence %d: bits (%d, %d) must each be 1, 2, 4 or 8", i, d->bits_k[i], d->bits_v[i]);
+  }
+  return KVQ_OK;
+}
+
+int64_t packed_capacity(const kvq_cache_desc* d) {
+  const int64_t past = (int64_t)d->max_tokens - d->fp16_window;
+  return past <= 0 ? 0 : past / d->key_group * d->key_group;
+}
+
+int32_t quantized_len(int64_t L, const kvq_cache_desc& d) {
+  const int64_t past = L - d.fp16_window;
+  return past <= 0 ? 0 : (int32_t)(past / d.key_group * d.key_group);
+}
+
+HeadLayout layout_of(const kvq_cache_desc* d, int bk, int bv) {
+  return kvq::head_layout(bk, bv, packed_capacity(d), d->key_group, d->value_group,
+                          (int64_t)d->fp16_window + d->key_group);
+}
+
+int32_t split_tokens_for(const kvq_cache* c) {
+  const int gk = c->d.key_group;
+  if (c->split_tokens > 0) return c->split_tokens;
+  int64_t total = 0, lq_max = 0;
+  for (int i = 0; i < c->d.batch; ++i) {
+    total += (int64_t)c->Lq[i] * c->d.num_kv_heads;
+    lq_max = std::max<int64_t>(lq_max, c->Lq[i]);
+  }
+  int64_t st = (total + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  st = std::max<int64_t>(st, (lq_max + kMaxSplits - 1) / kMaxSplits);
+  st = (st + gk - 1) / gk * gk;
+  st = std::max<int64_t>(st, (int64_t)gk * kMinGroupsPerSplit);
+  return (int32_t)std::min<int64_t>(st, (int64_t)1 << 30);
+}
+
+int64_t splits_bound(const kvq_cache* c) {
+  const int64_t cq = c->cq;
+  int64_t nq;
+  if (c->split_tokens > 0)
+    nq = (cq + c->split_tokens - 1) / c->split_tokens;
+  else
+    nq = std::min<int64_t>(kMaxSplits, (cq + (int64_t)c->d.key_group * kMinGroupsPerSplit - 1) /
+                                           ((int64_t)c->d.key_group * kMinGroupsPerSplit));
+  return nq + 1;
+}
+
+kvq_status hip_fail(int e, const char* what) {
+  return fail(KVQ_ERR_HIP, "%s: %s", what, hipGetErrorString((hipError_t)e));
+}
+
+// Sequences grouped by (key bits, value bits), each class in chunks that fit
+// one kernel-argument block.
+std::vector<std::pair<std::pair<int, int>, std::vector<int>>> bit_classes(const kvq_cache* c,
+                                                                          const std::vector<int>& seqs) {
+  std::map<std::pair<int, int>, std::vector<int>> m;
+  for (int i : seqs) m[{c->bk[i], c->bv[i]}].push_back(i);
+  std::vector<std::pair<std::pair<int, int>, std::vector<int>>> out;
+  for (auto& kv : m) {
+    for (size_t b = 0; b < kv.second.size(); b += kvq::kMaxSeqPerLaunch) {
+      const size_t e = std::min(kv.second.size(), b + kvq::kMaxSeqPerLaunch);
+      out.push_back({kv.first, std::vector<int>(kv.second.begin() + b, kv.second.begin() + e)});
+    }
+  }
+  return out;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t kvq_cache_bytes(const kvq_cache_desc* d) {
+  if (check_desc(d) != KVQ_OK) return 0;
+  uint64_t total = kvq::kHeaderBytes;
+  for (int i = 0; i < d->batch; ++i) total += (uint64_t)d->num_kv_heads * layout_of(d, d->bits_k[i], d->bits_v[i]).stride;
+  return (size_t)total;
+}
+
+kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena, size_t arena_bytes) {
+  if (!out) return fail(KVQ_ERR_ARG, "out is NULL");
+  *out = nullptr;
+  const kvq_status st = check_desc(d);
+  if (st != KVQ_OK) return st;
+  if (!arena) return fail(KVQ_ERR_ARG, "arena is NULL");
+  if (reinterpret_cast<uintptr_t>(arena) % kvq::kAlign != 0) return fail(KVQ_ERR_ARG, "arena must be 256-byte aligned");
+  const size_t need = kvq_cache_bytes(d);
+  if (arena_bytes < need)
+    return fail(KVQ_ERR_CAPACITY, "arena holds %zu bytes, the cache needs %zu", arena_bytes, need);
+  kvq_cache* c = new kvq_cache();
+  c->d = *d;
+  c->bk.assign(d->bits_k, d->bits_k + d->batch);
+  c->bv.assign(d->bits_v, d->bits_v + d->batch);
+  c->d.bits_k = c->bk.data();
+  c->d.bits_v = c->bv.data();
+  c->arena = static_cast<uint8_t*>(arena);
+  c->arena_bytes = arena_bytes;
+  c->cq = packed_capacity(d);
+  c->W = d->fp16_window + d->key_group;
+  uint64_t off = kvq::kHeaderBytes;
+  for (int i = 0; i < d->batch; ++i) {
+    c->lay.push_back(layout_of(d, c->bk[i], c->bv[i]));
+    c->head0.push_back(off);
+    off += (uint64_t)d->num_kv_heads * c->lay.back().stride;
+  }
+  c->L.assign(d->batch, 0);
+  c->Lq.assign(d->batch, 0);
+  *out = c;
+  return ok();
+}
+
+void kvq_cache_destroy(kvq_cache* c) { delete c; }
+
+kvq_status kvq_cache_reset(kvq_cache* c, void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  const int e = kvq::launch_fill_zero(c->arena, kvq::kHeaderBytes / 4, stream);
+  if (e) return hip_fail(e, "reset");
+  std::fill(c->L.begin(), c->L.end(), 0);
+  std::fill(c->Lq.begin(), c->Lq.end(), 0);
+  return ok();
+}
+
+int64_t kvq_seq_len(const kvq_cache* c, int32_t seq) {
+  if (!c || seq < 0 || seq >= c->d.batch) return -1;
+  return c->L[seq];
+}
+
+kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int32_t n_max, const int32_t* n_new,
+                      void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (!n_new) return fail(KVQ_ERR_ARG, "n_new is NULL");
+  if (n_max < 0) return fail(KVQ_ERR_ARG, "n_max must be >= 0");
+  const kvq_cache_desc& d = c->d;
+  bool any = false;
+  for (int i = 0; i < d.batch; ++i) {
+    if (n_new[i] < 0 || n_new[i] > n_max)
+      return fail(KVQ_ERR_ARG, "sequence %d: n_new = %d outside [0, n_max = %d]", i, n_new[i], n_max);
+    if ((int64_t)c->L[i] + n_new[i] > d.max_tokens)
+      return fail(KVQ_ERR_CAPACITY, "sequence %d: %d + %d tokens exceed max_tokens = %d", i, c->L[i], n_new[i],
+                  d.max_tokens);
+    any |= n_new[i] > 0;
+  }
+  if (!any) return ok();
+  if (!K || !V) return fail(KVQ_ERR_ARG, "K and V must be device pointers");
+
+  std::vector<int> seqs;
+  std::vector<int32_t> L_new(d.batch), Lq_new(d.batch);
+  bool fused = true;
+  for (int i = 0; i < d.batch; ++i) {
+    L_new[i] = c->L[i] + n_new[i];
+    Lq_new[i] = quantized_len(L_new[i], d);
+    if (n_new[i] > 0) seqs.push_back(i);
+    if ((int64_t)L_new[i] - c->Lq[i] > c->W) fused = false;
+  }
+
+  // fused: one launch packs groups and fills ring slots (no slot is both
+  // read and written); otherwise pack first, then fill the ring.
+  const int phases = fused ? 1 : 2;
+  for (int ph = 0; ph < phases; ++ph) {
+    const bool quant = fused || ph == 0, copy = fused || ph == 1;
+    for (auto& cls : bit_classes(c, seqs)) {
+      kvq::AppendArgs a{};
+      const HeadLayout& lay = c->lay[cls.second[0]];
+      a.arena = c->arena;
+      a.K = static_cast<const uint16_t*>(K);
+      a.V = static_cast<const uint16_t*>(V);
+      a.head_stride = lay.stride;
+      a.kc = (uint32_t)lay.kc; a.km = (uint32_t)lay.km; a.vc = (uint32_t)lay.vc;
+      a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
+      a.n_max = n_max; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
+      a.quantize = quant ? 1 : 0;
+      int wg = 0, n = 0;
+      for (int i : cls.second) {
+        kvq::AppendSeq& s = a.seq[n++];
+        s.head0 = c->head0[i];
+        s.seq = i;
+        s.L_old = c->L[i]; s.Lq_old = c->Lq[i]; s.L_new = L_new[i]; s.Lq_new = Lq_new[i];
+        s.n_quant = (Lq_new[i] - c->Lq[i]) / d.key_group;
+        s.do_copy = (copy && L_new[i] > std::max(Lq_new[i], c->L[i])) ? 1 : 0;
+        s.wg_begin = wg;
+        wg += (quant ? s.n_quant * d.num_kv_heads : 0) + (s.do_copy ? d.num_kv_heads : 0);
+      }
+      a.nseq = n;
+      a.total_wg = wg;
+      const int e = kvq::launch_append(a, cls.first.first, cls.first.second, stream);
+      if (e) return hip_fail(e, "append launch");
+    }
+  }
+  for (int i = 0; i < d.batch; ++i) {
+    c->L[i] = L_new[i];
+    c->Lq[i] = Lq_new[i];
+  }
+  return ok();
+}
+
+size_t kvq_workspace_bytes(const kvq_cache* c) {
+  if (!c) return 0;
+  return (size_t)c->d.batch * c->d.num_q_heads * (size_t)splits_bound(c) * kvq::kRecFloats * sizeof(float);
+}
+
+namespace {
+
+struct SplitPlan {
+  int32_t split_tokens = 0;
+  std::vector<int32_t> nq, ns, base;
+  int64_t records = 0;
+};
+
+SplitPlan plan_splits(const kvq_cache* c) {
+  SplitPlan p;
+  const int B = c->d.batch;
+  p.split_tokens = split_tokens_for(c);
+  p.nq.resize(B);
+  p.ns.resize(B);
+  p.base.resize(B);
+  for (int i = 0; i < B; ++i) {
+    p.nq[i] = (c->Lq[i] + p.split_tokens - 1) / p.split_tokens;
+    p.ns[i] = p.nq[i] + (c->L[i] > c->Lq[i] ? 1 : 0);
+    p.base[i] = (int32_t)p.records;
+    p.records += p.ns[i];
+  }
+  return p;
+}
+
+kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, void* ws, size_t ws_bytes,
+                        void* stream) {
+  const kvq_cache_desc& d = c->d;
+  const size_t need = (size_t)p.records * d.num_q_heads * kvq::kRecFloats * sizeof(float);
+  if (!q) return fail(KVQ_ERR_ARG, "q must be a device pointer");
+  if (need > 0 && !ws) return fail(KVQ_ERR_ARG, "workspace is NULL");
+  if (ws_bytes < need) return fail(KVQ_ERR_CAPACITY, "workspace holds %zu bytes, this call needs %zu", ws_bytes, need);
+  if (reinterpret_cast<uintptr_t>(ws) % 16 != 0) return fail(KVQ_ERR_ARG, "workspace must be 16-byte aligned");
+  std::vector<int> seqs;
+  for (int i = 0; i < d.batch; ++i)
+    if (c->L[i] > 0) seqs.push_back(i);
+  const float qscale = (float)(1.4426950408889634 / std::sqrt((double)d.head_dim));
+  for (auto& cls : bit_classes(c, seqs)) {
+    kvq::DecodeArgs a{};
+    const HeadLayout& lay = c->lay[cls.second[0]];
+    a.arena = c->arena;
+    a.q = static_cast<const uint16_t*>(q);
+    a.ws = static_cast<float*>(ws);
+    a.head_stride = lay.stride;
+    a.kc = (uint32_t)lay.kc; a.km = (uint32_t)lay.km; a.vc = (uint32_t)lay.vc;
+    a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
+    a.hq = d.num_q_heads; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
+    a.split_tokens = p.split_tokens;
+    a.qscale = qscale;
+    int wg = 0, n = 0;
+    for (int i : cls.second) {
+      kvq::DecodeSeq& s = a.seq[n++];
+      s.head0 = c->head0[i];
+      s.seq = i; s.L = c->L[i]; s.Lq = c->Lq[i];
+      s.nq = p.nq[i]; s.nsplit = p.ns[i]; s.ws_base = p.base[i];
+      s.wg_begin = wg;
+      wg += p.ns[i] * d.num_kv_heads;
+    }
+    a.nseq = n;
+    a.total_wg = wg;
+    const int e = kvq::launch_decode(a, cls.first.first, cls.first.second, d.num_q_heads / d.num_kv_heads, stream);
+    if (e) return hip_fail(e, "decode launch");
+  }
+  return KVQ_OK;
+}
+
+kvq_status run_merge(const kvq_cache* c, const SplitPlan& p, const void* ws, float* out, void* stream) {
+  const kvq_cache_desc& d = c->d;
+  if (!out) return fail(KVQ_ERR_ARG, "out must be a device pointer");
+  if (p.records > 0 && !ws) return fail(KVQ_ERR_ARG, "workspace is NULL");
+  for (int b = 0; b < d.batch; b += kvq::kMaxSeqPerLaunch) {
+    kvq::MergeArgs m{};
+    m.ws = static_cast<const float*>(ws);
+    m.out = out;
+    m.hq = d.num_q_heads;
+    int n = 0;
+    for (int i = b; i < std::min(d.batch, b + kvq::kMaxSeqPerLaunch); ++i) {
+      m.seq[n].seq = i; m.seq[n].nsplit = p.ns[i]; m.seq[n].ws_base = p.base[i];
+      ++n;
+    }
+    m.nseq = n;
+    const int e = kvq::launch_merge(m, stream);
+    if (e) return hip_fail(e, "merge launch");
+  }
+  return KVQ_OK;
+}
+
+}  // namespace
+
+kvq_status kvq_decode_attention(const kvq_cache* c, const void* q, float* out, void* ws, size_t ws_bytes,
+                                void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (!q || !out) return fail(KVQ_ERR_ARG, "q and out must be device pointers");
+  const SplitPlan p = plan_splits(c);
+  kvq_status st = run_partials(c, p, q, ws, ws_bytes, stream);
+  if (st != KVQ_OK) return st;
+  st = run_merge(c, p, ws, out, stream);
+  if (st != KVQ_OK) return st;
+  return ok();
+}
+
+kvq_status kvq_decode_partials(const kvq_cache* c, const void* q, void* ws, size_t ws_bytes, void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  const kvq_status st = run_partials(c, plan_splits(c), q, ws, ws_bytes, stream);
+  return st == KVQ_OK ? ok() : st;
+}
+
+kvq_status kvq_decode_merge(const kvq_cache* c, const void* ws, float* out, void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  const kvq_status st = run_merge(c, plan_splits(c), ws, out, stream);
+  return st == KVQ_OK ? ok() : st;
+}
+
+kvq_status kvq_dequant(const kvq_cache* c, int32_t seq, int32_t tok0, int32_t ntok, float* K_out, float* V_out,
+                       void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (seq < 0 || seq >= c->d.batch) return fail(KVQ_ERR_ARG, "seq %d out of range", seq);
+  if (tok0 < 0 || ntok < 0 || (int64_t)tok0 + ntok > c->L[seq])
+    return fail(KVQ_ERR_ARG, "token range [%d, %lld) outside [0, %d)", tok0, (long long)tok0 + ntok, c->L[seq]);
+  if (ntok == 0) return ok();
+  if (!K_out || !V_out) return fail(KVQ_ERR_ARG, "outputs must be device pointers");
+  const HeadLayout& lay = c->lay[seq];
+  kvq::DequantArgs a{};
+  a.base = c->arena + c->head0[seq];
+  a.K_out = K_out; a.V_out = V_out;
+  a.head_stride = lay.stride;
+  a.kc = (uint32_t)lay.kc; a.km = (uint32_t)lay.km; a.vc = (uint32_t)lay.vc;
+  a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
+  a.hkv = c->d.num_kv_heads; a.gk = c->d.key_group; a.gv = c->d.value_group; a.W = c->W;
+  a.bk = c->bk[seq]; a.bv = c->bv[seq]; a.Lq = c->Lq[seq]; a.tok0 = tok0; a.ntok = ntok;
+  const int e = kvq::launch_dequant(a, stream);
+  if (e) return hip_fail(e, "dequant launch");
+  return ok();
+}
+
+size_t kvq_export_bytes(const kvq_cache* c, int32_t seq, int32_t h) {
+  if (!c || seq < 0 || seq >= c->d.batch || h < 0 || h >= c->d.num_kv_heads) return 0;
+  const size_t Lq = c->Lq[seq], tail = c->L[seq] - c->Lq[seq], D = kvq::kHeadDim;
+  return Lq * 16 * c->bk[seq] + Lq / c->d.key_group * 2 * D * 2 + Lq * 16 * c->bv[seq] +
+         Lq * (D / c->d.value_group) * 4 + tail * D * 2 * 2;
+}
+
+kvq_status kvq_export(const kvq_cache* c, int32_t seq, int32_t h, void* dst, size_t bytes, void* stream) {
+  const size_t need = kvq_export_bytes(c, seq, h);
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (seq < 0 || seq >= c->d.batch || h < 0 || h >= c->d.num_kv_heads)
+    return fail(KVQ_ERR_ARG, "(seq %d, kv head %d) out of range", seq, h);
+  if (bytes < need) return fail(KVQ_ERR_CAPACITY, "destination holds %zu bytes, the image has %zu", bytes, need);
+  if (need == 0) return ok();
+  if (!dst) return fail(KVQ_ERR_ARG, "destination is NULL");
+  const HeadLayout& lay = c->lay[seq];
+  const uint8_t* blk = c->arena + c->head0[seq] + (uint64_t)h * lay.stride;
+  uint8_t* o = static_cast<uint8_t*>(dst);
+  const size_t Lq = c->Lq[seq], L = c->L[seq], D = kvq::kHeadDim;
+  const size_t part[4][2] = {{lay.kc, Lq * 16 * c->bk[seq]},
+                             {lay.km, Lq / c->d.key_group * 2 * D * 2},
+                             {lay.vc, Lq * 16 * c->bv[seq]},
+                             {lay.vm, Lq * (D / c->d.value_group) * 4}};
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (auto& p : part) {
+    if (p[1] == 0) continue;
+    const hipError_t e = hipMemcpyAsync(o, blk + p[0], p[1], hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "export copy");
+    o += p[1];
+  }
+  const size_t W = c->W, n = L - Lq, first = Lq % W;
+  for (uint64_t ring : {lay.tk, lay.tv}) {
+    const size_t a1 = std::min(n, W - first), a2 = n - a1;
+    if (a1) {
+      const hipError_t e = hipMemcpyAsync(o, blk + ring + first * D * 2, a1 * D * 2, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return hip_fail(e, "export copy");
+      o += a1 * D * 2;
+    }
+    if (a2) {
+      const hipError_t e = hipMemcpyAsync(o, blk + ring, a2 * D * 2, hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return hip_fail(e, "export copy");
+      o += a2 * D * 2;
+    }
+  }
+  return ok();
+}
+
+kvq_status kvq_check(const kvq_cache* c, void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "stream synchronize");
+  uint32_t flag = 0;
+  e = hipMemcpy(&flag, c->arena, sizeof flag, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "read error flag");
+  if (flag == (uint32_t)KVQ_ERR_RANGE)
+    return fail(KVQ_ERR_RANGE, "an append met a non-finite input or a group range beyond the fp16 scale");
+  return ok();
+}
+
+kvq_status kvq_set_split_tokens(kvq_cache* c, int32_t tokens) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (tokens < 0 || (tokens > 0 && tokens % c->d.key_group != 0))
+    return fail(KVQ_ERR_ARG, "split tokens %d must be 0 or a positive multiple of key_group %d", tokens,
+                c->d.key_group);
+  c->split_tokens = tokens;
+  return ok();
+}
+
+const char* kvq_last_error(void) { return g_err.c_str(); }
+
+const char* kvq_version(void) { return "kvq 0.1.0 gfx950"; }
+
+}  // extern "C"

@@ -1,0 +1,126 @@
+// Internal definitions shared by the host library and the HIP kernels.
+//
+// Device arena:
+//   [0, 256)            header; word 0 is the sticky error flag
+//   per sequence i, per kv head h, one block of head_stride(i) bytes:
+//     kc  key codes    [Cq][16*bk]       token rows, canonical bit order
+//     km  key meta     [Cq/Gk][2][128]   fp16 scales then zeros per key group
+//     vc  value codes  [Cq][16*bv]
+//     vm  value meta   [Cq][128/Gv][2]   fp16 (scale, zero) per value group
+//     tk  key ring     [W][128]          fp16 tokens not yet packed
+//     tv  value ring   [W][128]
+//   Cq = Gk * floor(max(0, L_max - R) / Gk) is the most tokens ever packed;
+//   W = R + Gk ring slots hold the < R + Gk fp16 tokens, token p in slot p % W.
+//   Every region starts on a 256-byte boundary.
+//
+// The packed regions use the canonical byte order of the export image, so an
+// export is a handful of device-to-device copies.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kvq {
+
+constexpr int kHeadDim = 128;
+constexpr int kMaxSeqPerLaunch = 64;   // sequences described in one kernel-argument block
+constexpr int kRecFloats = 132;        // split record: m, l, 2 pad, acc[128]
+constexpr uint64_t kAlign = 256;
+constexpr uint64_t kHeaderBytes = 256;
+
+inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+struct HeadLayout {
+  uint64_t kc, km, vc, vm, tk, tv;  // byte offsets inside a (seq, head) block
+  uint64_t stride;                  // block size
+};
+
+inline HeadLayout head_layout(int bk, int bv, int64_t cq, int gk, int gv, int64_t w) {
+  HeadLayout L{};
+  uint64_t o = 0;
+  L.kc = o; o = align_up(o + (uint64_t)cq * 16 * bk, kAlign);
+  L.km = o; o = align_up(o + (uint64_t)(cq / gk) * 2 * kHeadDim * 2, kAlign);
+  L.vc = o; o = align_up(o + (uint64_t)cq * 16 * bv, kAlign);
+  L.vm = o; o = align_up(o + (uint64_t)cq * (kHeadDim / gv) * 4, kAlign);
+  L.tk = o; o = align_up(o + (uint64_t)w * kHeadDim * 2, kAlign);
+  L.tv = o; o = align_up(o + (uint64_t)w * kHeadDim * 2, kAlign);
+  L.stride = o;
+  return L;
+}
+
+// ---------------------------------------------------------------- append
+
+struct AppendSeq {
+  uint64_t head0;     // arena offset of (seq, head 0)
+  int32_t seq;        // index into the input batch
+  int32_t L_old, Lq_old, Lq_new, L_new;
+  int32_t wg_begin;   // first workgroup of this sequence
+  int32_t n_quant;    // key groups to pack per head
+  int32_t do_copy;    // 1 if this launch writes ring slots
+};
+
+struct AppendArgs {
+  uint8_t* arena;
+  const uint16_t* K;  // fp16 [batch][n_max][Hkv][128]
+  const uint16_t* V;
+  uint64_t head_stride;
+  uint32_t kc, km, vc, vm, tk, tv;
+  int32_t n_max, hkv, gk, gv, W, nseq, total_wg;
+  int32_t quantize;   // 1: pack groups in this launch
+  AppendSeq seq[kMaxSeqPerLaunch];
+};
+
+// ---------------------------------------------------------------- decode
+
+struct DecodeSeq {
+  uint64_t head0;
+  int32_t seq;        // batch index (q / out row)
+  int32_t L, Lq;
+  int32_t nq;         // packed splits per head
+  int32_t nsplit;     // nq + (L > Lq)
+  int32_t wg_begin;
+  int32_t ws_base;    // first split record of this sequence
+  int32_t pad;
+};
+
+struct DecodeArgs {
+  const uint8_t* arena;
+  const uint16_t* q;  // fp16 [batch][Hq][128]
+  float* ws;          // split records [.][Hq][kRecFloats]
+  uint64_t head_stride;
+  uint32_t kc, km, vc, vm, tk, tv;
+  int32_t hq, hkv, gk, gv, W, split_tokens, nseq, total_wg;
+  float qscale;       // log2(e) / sqrt(d)
+  DecodeSeq seq[kMaxSeqPerLaunch];
+};
+
+struct MergeSeq {
+  int32_t seq, nsplit, ws_base, pad;
+};
+
+struct MergeArgs {
+  const float* ws;
+  float* out;         // fp32 [batch][Hq][128]
+  int32_t hq, nseq;
+  MergeSeq seq[kMaxSeqPerLaunch];
+};
+
+// ---------------------------------------------------------------- dequant
+
+struct DequantArgs {
+  const uint8_t* base;  // (seq, head 0) block
+  float* K_out;
+  float* V_out;
+  uint64_t head_stride;
+  uint32_t kc, km, vc, vm, tk, tv;
+  int32_t hkv, gk, gv, W, bk, bv, Lq, tok0, ntok;
+};
+
+// Launchers (defined next to their kernels).  Return a hipError_t as int.
+int launch_append(const AppendArgs& a, int bk, int bv, void* stream);
+int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
+int launch_merge(const MergeArgs& a, void* stream);
+int launch_dequant(const DequantArgs& a, void* stream);
+int launch_fill_zero(void* dst, size_t words, void* stream);
+
+}  // namespace kvq

@@ -1,0 +1,158 @@
+"""Host-side tests of the C-ABI library (no GPU needed).
+
+The library loads, exports every function include/kvq.h declares, sizes its
+arena as documented, and rejects bad arguments before touching any device
+memory, leaving the cache unchanged.
+"""
+import os
+import re
+
+import pytest
+
+from paper_2607_16248_amd import kvq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE_ARENA = 1 << 30   # a 256-aligned address that is never dereferenced on these paths
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "kvq.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvq_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = kvq.lib()
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(names) == sorted(kvq.EXPORTED)
+    assert "gfx950" in kvq.kvq_version()
+
+
+def align(x, a=256):
+    return (x + a - 1) // a * a
+
+
+def expected_bytes(batch, hkv, max_tokens, gk, gv, R, bits_k, bits_v):
+    """Arena size from the documented region list, written out independently."""
+    cq = max(0, max_tokens - R) // gk * gk
+    W = R + gk
+    total = 256
+    for bk, bv in zip(bits_k, bits_v):
+        per_head = (align(cq * 16 * bk) + align(cq // gk * 512) + align(cq * 16 * bv)
+                    + align(cq * (128 // gv) * 4) + 2 * align(W * 256))
+        total += hkv * per_head
+    return total
+
+
+@pytest.mark.parametrize("args", [
+    (1, 32, 8, 4096, 32, 32, 0, [2], [2]),
+    (1, 32, 8, 131072, 32, 32, 0, [1], [1]),
+    (16, 32, 8, 32768, 64, 32, 0, [2] * 8 + [4] * 8, [2] * 8 + [4] * 8),
+    (4, 40, 8, 131072, 32, 32, 128, [8] * 4, [8] * 4),
+    (3, 8, 8, 100, 128, 8, 300, [1, 2, 4], [8, 4, 1]),
+])
+def test_cache_bytes(args):
+    b, hq, hkv, L, gk, gv, R, bk, bv = args
+    d = kvq.make_desc(b, hq, hkv, 128, L, gk, gv, R, bk, bv)
+    assert kvq.kvq_cache_bytes(d) == expected_bytes(b, hkv, L, gk, gv, R, bk, bv)
+
+
+BAD = [
+    (dict(batch=0), kvq.ERR_ARG),
+    (dict(num_kv_heads=0), kvq.ERR_ARG),
+    (dict(num_q_heads=12), kvq.ERR_ARG),          # not a multiple of 8
+    (dict(num_q_heads=24), kvq.ERR_UNSUPPORTED),  # 3 query heads per kv head
+    (dict(head_dim=64), kvq.ERR_UNSUPPORTED),
+    (dict(head_dim=0), kvq.ERR_ARG),
+    (dict(max_tokens=0), kvq.ERR_ARG),
+    (dict(key_group=16), kvq.ERR_ARG),
+    (dict(key_group=48), kvq.ERR_ARG),
+    (dict(value_group=24), kvq.ERR_ARG),
+    (dict(fp16_window=-1), kvq.ERR_ARG),
+    (dict(bits_k=[3]), kvq.ERR_ARG),
+    (dict(bits_v=[0]), kvq.ERR_ARG),
+]
+
+
+def desc(**kw):
+    p = dict(batch=1, num_q_heads=32, num_kv_heads=8, head_dim=128, max_tokens=4096, key_group=32,
+             value_group=32, fp16_window=0, bits_k=[2], bits_v=[2])
+    p.update(kw)
+    return kvq.make_desc(**p)
+
+
+@pytest.mark.parametrize("kw,status", BAD)
+def test_invalid_descriptors(kw, status):
+    d = desc(**kw)
+    assert kvq.kvq_cache_bytes(d) == 0
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.kvq_cache_init(d, FAKE_ARENA, 1 << 40)
+    assert e.value.status == status
+    assert kvq.kvq_last_error() != ""
+
+
+def test_init_checks_arena():
+    d = desc()
+    n = kvq.kvq_cache_bytes(d)
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.kvq_cache_init(d, FAKE_ARENA, n - 1)
+    assert e.value.status == kvq.ERR_CAPACITY
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.kvq_cache_init(d, FAKE_ARENA + 16, n)
+    assert e.value.status == kvq.ERR_ARG
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.kvq_cache_init(d, None, n)
+    assert e.value.status == kvq.ERR_ARG
+    h = kvq.kvq_cache_init(d, FAKE_ARENA, n)
+    assert kvq.kvq_last_error() == ""
+    kvq.kvq_cache_destroy(h)
+
+
+def test_append_errors_leave_cache_unchanged():
+    d = desc(batch=2, bits_k=[1, 4], bits_v=[1, 4], max_tokens=100)
+    h = kvq.kvq_cache_init(d, FAKE_ARENA, kvq.kvq_cache_bytes(d))
+    try:
+        for n_new, n_max, status in [([101, 0], 200, kvq.ERR_CAPACITY), ([5, -1], 10, kvq.ERR_ARG),
+                                     ([11, 0], 10, kvq.ERR_ARG), ([0, 0], -1, kvq.ERR_ARG)]:
+            with pytest.raises(kvq.KvqError) as e:
+                kvq.kvq_append(h, FAKE_ARENA, FAKE_ARENA, n_new, n_max=n_max)
+            assert e.value.status == status
+            assert kvq.kvq_seq_len(h, 0) == 0 and kvq.kvq_seq_len(h, 1) == 0
+        # nothing to append: a no-op that launches nothing
+        kvq.kvq_append(h, None, None, [0, 0], n_max=0)
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.kvq_append(h, None, None, [1, 0], n_max=1)
+        assert e.value.status == kvq.ERR_ARG
+        assert kvq.kvq_seq_len(h, 2) == -1 and kvq.kvq_seq_len(h, -1) == -1
+    finally:
+        kvq.kvq_cache_destroy(h)
+
+
+def test_split_setting_and_workspace_bound():
+    d = desc(max_tokens=131072, bits_k=[1], bits_v=[1])
+    h = kvq.kvq_cache_init(d, FAKE_ARENA, kvq.kvq_cache_bytes(d))
+    try:
+        rec = 132 * 4
+        # automatic: at most 512 packed splits (and >= 4 key groups each) + one tail split
+        assert kvq.kvq_workspace_bytes(h) == 32 * (min(512, 131072 // 128) + 1) * rec
+        kvq.kvq_set_split_tokens(h, 1024)
+        assert kvq.kvq_workspace_bytes(h) == 32 * (128 + 1) * rec
+        for bad in (-32, 33, 100):
+            with pytest.raises(kvq.KvqError) as e:
+                kvq.kvq_set_split_tokens(h, bad)
+            assert e.value.status == kvq.ERR_ARG
+        kvq.kvq_set_split_tokens(h, 0)
+        # an empty cache exports nothing
+        assert kvq.kvq_export_bytes(h, 0, 0) == 0
+        assert kvq.kvq_export_bytes(h, 0, 8) == 0 and kvq.kvq_export_bytes(h, 1, 0) == 0
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.kvq_dequant(h, 0, 0, 1, FAKE_ARENA, FAKE_ARENA)
+        assert e.value.status == kvq.ERR_ARG
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.kvq_decode_attention(h, None, None, None)
+        assert e.value.status == kvq.ERR_ARG
+    finally:
+        kvq.kvq_cache_destroy(h)

@@ -1,0 +1,203 @@
+"""GPU parity: the HIP library against the CPU oracle, through the C ABI.
+
+- packed codes, scales, zeros and fp16 tail: byte-identical to the oracle's
+  canonical image (kvq_export), after one-shot and piecewise appends;
+- kvq_dequant: bit-identical to the oracle's exact value rounded to fp32;
+- decode attention: row-normwise relative error <= 2e-3 against the fp64
+  oracle on the same (byte-identical) cache;
+- properties: split-count independence, bitwise determinism, empty and
+  single-token sequences, ragged batches with mixed bit widths, the device
+  error flag.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from helpers import ATTN_TOL, Case, log, row_rel_err
+from workloads import Workload, workload
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def W(name, batch, hq, hkv, lens, bk, bv, gk=32, gv=32, R=0, dist="normal", cfg=90):
+    if isinstance(lens, int):
+        lens = (lens,) * batch
+    if isinstance(bk, int):
+        bk = (bk,) * batch
+    if isinstance(bv, int):
+        bv = (bv,) * batch
+    return Workload(name, batch, hq, hkv, 128, tuple(lens), tuple(bk), tuple(bv), gk, gv, R,
+                    key_dist=dist, cfg_id=cfg)
+
+
+SMALL = [
+    W("k2v2_g32_L1000", 1, 32, 8, 1000, 2, 2),
+    W("k1v1_g32_L2048", 1, 32, 8, 2048, 1, 1),
+    W("k4v4_g32_L1111", 1, 32, 8, 1111, 4, 4),
+    W("k8v8_g32_L777", 1, 32, 8, 777, 8, 8),
+    W("k2v1_g32_L999", 1, 32, 8, 999, 2, 1),
+    W("k1v2_g32_L999", 1, 32, 8, 999, 1, 2),
+    W("k4v8_g64_gv8_L1300", 1, 16, 4, 1300, 4, 8, gk=64, gv=8),
+    W("k1v4_g128_gv128_L1500", 1, 8, 8, 1500, 1, 4, gk=128, gv=128),
+    W("gq5_k2v2_R128_t3", 2, 40, 8, (1000, 517), 2, 2, R=128, dist="student_t3"),
+    W("gq2_k1v1_R40", 1, 16, 8, 333, 1, 1, R=40),
+    W("gq8_k8v8_gv16", 1, 64, 8, 600, 8, 8, gv=16),
+    W("ragged_mixed", 4, 32, 8, (900, 64, 31, 1500), (2, 2, 4, 4), (2, 2, 4, 4), gk=64),
+    W("window_bigger_than_L", 1, 32, 8, 100, 1, 1, R=300),
+]
+
+
+@pytest.mark.parametrize("w", SMALL, ids=[w.name for w in SMALL])
+def test_bytes_and_attention_match_oracle(w):
+    log(f"[parity] {w.name}: append")
+    c = Case(w)
+    c.append_all()
+    c.cache.check()
+    for s in range(w.batch):
+        for h in range(w.num_kv_heads):
+            got = c.cache.export(s, h)
+            ref = c.oracle_image(s, h)
+            assert got.size == ref.size, (s, h)
+            bad = np.flatnonzero(got != ref)
+            assert bad.size == 0, f"seq {s} head {h}: {bad.size} bytes differ, first at {bad[:5]}"
+    log(f"[parity] {w.name}: decode")
+    out = c.decode()
+    worst = 0.0
+    for s in range(w.batch):
+        ref = c.oracle_out(s)
+        err = row_rel_err(out[s], ref)
+        worst = max(worst, float(err.max()))
+        assert err.max() <= ATTN_TOL, (s, err.max())
+    log(f"[parity] {w.name}: max row-relative error {worst:.3e}")
+
+
+@pytest.mark.parametrize("chunks", [
+    [1] * 70,                        # token by token across two key-group flushes
+    [5, 31, 32, 33, 64, 1, 100],     # ragged chunks crossing group edges
+    [300],                           # prefill larger than ring + window
+])
+def test_piecewise_appends_give_the_same_bytes(chunks):
+    L = sum(chunks)
+    w = W(f"pieces_{L}", 2, 32, 8, (L, max(1, L - 7)), 2, 2, R=40)
+    c = Case(w)
+    log(f"[append] chunks {chunks[:8]}...")
+    c.append_all(chunks)
+    c.cache.check()
+    for s in range(2):
+        for h in (0, 5):
+            assert (c.cache.export(s, h) == c.oracle_image(s, h)).all(), (s, h)
+    out = c.decode()
+    for s in range(2):
+        assert row_rel_err(out[s], c.oracle_out(s)).max() <= ATTN_TOL
+
+
+def test_dequant_is_bit_exact():
+    w = W("dq", 2, 32, 8, (700, 450), (1, 4), (2, 8), gk=64, gv=16, R=50)
+    c = Case(w)
+    c.append_all()
+    for s in range(2):
+        L = w.lens[s]
+        Kd, Vd = c.cache.dequant(s, 0, L)
+        Kd, Vd = Kd.cpu().numpy(), Vd.cpu().numpy()
+        for h in range(w.num_kv_heads):
+            Kh, Vh = oracle.dequant_head(c.oracle_image(s, h), L, 128, w.bits_k[s], w.bits_v[s],
+                                         w.key_group, w.value_group, w.window)
+            assert (Kd[:, h].view(np.uint32) == Kh.astype(np.float32).view(np.uint32)).all(), (s, h)
+            assert (Vd[:, h].view(np.uint32) == Vh.astype(np.float32).view(np.uint32)).all(), (s, h)
+        # a sub-range starting mid-group
+        Kd2, _ = c.cache.dequant(s, 37, 100)
+        assert (Kd2.cpu().numpy() == Kd[37:137]).all()
+
+
+def test_split_independence_and_determinism():
+    w = W("splits", 1, 32, 8, 4100, 2, 2, R=3)
+    c = Case(w)
+    c.append_all()
+    ref = c.oracle_out(0)
+    outs = {}
+    for st in (128, 256, 1024, 4096, 0):
+        kvq_set = __import__("paper_2607_16248_amd").kvq_set_split_tokens
+        kvq_set(c.cache.handle, st)
+        a = c.decode()
+        b = c.decode()
+        assert (a.view(np.uint32) == b.view(np.uint32)).all(), st     # bitwise reproducible
+        assert row_rel_err(a[0], ref).max() <= ATTN_TOL, st
+        outs[st] = a
+    for st, a in outs.items():
+        assert row_rel_err(a[0], outs[128][0].astype(np.float64)).max() <= ATTN_TOL
+
+
+def test_empty_and_single_token_sequences():
+    w = W("tiny", 3, 32, 8, (0, 1, 40), 1, 1)
+    c = Case(w)
+    c.append_all()
+    out = c.decode()
+    assert (out[0] == 0).all()                          # no tokens: zeros
+    gq = 4
+    for h in range(32):                                 # one fp16 token: its value row, exactly
+        assert (out[1, h] == c.V[1][0, h // gq].astype(np.float32)).all()
+    assert row_rel_err(out[2], c.oracle_out(2)).max() <= ATTN_TOL
+
+
+def test_range_flag_is_sticky_until_reset():
+    from paper_2607_16248_amd import KvqError
+    from paper_2607_16248_amd.kvq import ERR_RANGE
+    cache = __import__("paper_2607_16248_amd").KVCache(1, 8, 8, 64, [1], [1])
+    K = torch.zeros((1, 32, 8, 128), dtype=torch.float16, device="cuda")
+    K[0, 0, 3, 7] = 65504.0
+    K[0, 1, 3, 7] = -65504.0                            # range 131008 > largest fp16 at one bit
+    V = torch.zeros_like(K)
+    cache.append(K, V)
+    with pytest.raises(KvqError) as e:
+        cache.check()
+    assert e.value.status == ERR_RANGE
+    cache.reset()
+    cache.check()
+    assert cache.seq_len(0) == 0
+
+
+# ------------------------------------------------ full-size workloads (sampled)
+
+def _sampled_parity(w, samples, layer=0):
+    heads = sorted({h for _, h in samples})
+    log(f"[full] {w.name}: generate heads {heads}")
+    c = Case(w, layer=layer, heads=heads)
+    log(f"[full] {w.name}: append")
+    c.append_all()
+    c.cache.check()
+    log(f"[full] {w.name}: decode")
+    out = c.decode()
+    gq = w.group_q
+    for s, h in samples:
+        assert (c.cache.export(s, h) == c.oracle_image(s, h)).all(), (s, h)
+        ref = c.oracle_out(s, heads=[h])
+        err = row_rel_err(out[s, h * gq:(h + 1) * gq], ref[h * gq:(h + 1) * gq])
+        log(f"[full] {w.name}: seq {s} head {h} max row-relative error {err.max():.3e}")
+        assert err.max() <= ATTN_TOL
+
+
+def test_full_workload_0_all_heads():
+    w = workload(0)
+    _sampled_parity(w, [(0, h) for h in range(8)])
+
+
+def test_full_workload_1_all_heads():
+    w = workload(1)
+    _sampled_parity(w, [(0, h) for h in range(8)])
+
+
+def test_full_workload_2_one_layer():
+    w = workload(2)
+    _sampled_parity(w, [(0, 0), (0, 5)], layer=7)
+
+
+def test_full_workload_3_sampled():
+    w = workload(3)
+    _sampled_parity(w, [(2, 1), (13, 6)])
+
+
+@pytest.mark.parametrize("bits", [1, 2, 4, 8])
+def test_full_workload_4_sampled(bits):
+    w = workload(4, bits)
+    _sampled_parity(w, [(0, 3), (3, 6)])
