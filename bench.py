@@ -119,6 +119,7 @@ def main():
               f"part of this library", file=sys.stderr, flush=True)
         sys.exit(2)
 
+    import numpy as np
     import torch
 
     from paper_2607_16248_amd import kvq
@@ -130,7 +131,6 @@ def main():
     w = workload(args.workload, args.bits)
     steps, warm = args.steps, args.warmup
     appending = args.workload == 2
-    per_layer = max(packed_bytes(L, w, bk, bv) for L, bk, bv in zip(w.lens, w.bits_k, w.bits_v))
     layers = w.layers if w.layers > 1 else max(1, min(64, -(-(1 << 30) // max(1, sum(
         packed_bytes(L, w, bk, bv) for L, bk, bv in zip(w.lens, w.bits_k, w.bits_v))))))
     extra = (steps + warm + 2) if appending else 0
@@ -151,7 +151,6 @@ def main():
             del K, V
         c.append(Kb, Vb, list(w.lens))
         del Kb, Vb
-        import numpy as np
         qs.append(torch.from_numpy(np.stack([gen_q(w, l, s) for s in range(w.batch)])).to(dev))
         outs.append(torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev))
         caches.append(c)
@@ -233,7 +232,7 @@ def main():
     launch_bytes = sum(packed_bytes(L, w, bk, bv) for L, bk, bv in zip(L_now, w.bits_k, w.bits_v))
     achieved = launch_bytes / (split_us * 1e-6) / 1e9
 
-    value = moved / (step_ms * 1e-3) / 1e9
+    value = moved / (step_ms * steps * 1e-3) / 1e9
     us_per_layer = step_ms * 1e3 / layers
     traffic_name = f"decode_split_{w.name}_traffic.txt"
     traffic = read_traffic(traffic_name)

@@ -114,7 +114,7 @@ size_t kvq_workspace_bytes(const kvq_cache* cache);
  * with kv(h) = h / (Hq / Hkv), K^ and V^ the dequantized cache (fp16 tail
  * tokens exact).  q: device fp16 [batch][Hq][d].  out: device fp32
  * [batch][Hq][d].  ws: device scratch of ws_bytes >= kvq_workspace_bytes,
- * 256-byte aligned, contents undefined on entry and exit.  A sequence with
+ * 16-byte aligned, contents undefined on entry and exit.  A sequence with
  * no tokens yields zeros.  Split-K over tokens (flash-decoding) followed
  * by a merge pass; results do not depend on the stream or on other
  * sequences, and are bitwise reproducible for a fixed split setting. */
@@ -162,9 +162,10 @@ kvq_status kvq_export(const kvq_cache* cache, int32_t seq, int32_t kv_head, void
  * else KVQ_OK.  The flag is sticky until kvq_cache_reset. */
 kvq_status kvq_check(const kvq_cache* cache, void* stream);
 
-/* Tokens per split of the decode kernel: a positive multiple of key_group,
- * or 0 to let the library choose from the current lengths (the default).
- * Changing it changes kvq_workspace_bytes. */
+/* Tokens per split of the decode kernel: a positive multiple of key_group
+ * giving at most 512 splits per sequence at capacity, or 0 to let the
+ * library choose from the current lengths (the default).  Changing it
+ * changes kvq_workspace_bytes. */
 kvq_status kvq_set_split_tokens(kvq_cache* cache, int32_t tokens);
 
 /* Message for the last non-OK status on this thread ("" if none). */

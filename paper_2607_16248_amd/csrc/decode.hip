@@ -342,24 +342,60 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   }
 }
 
-__global__ __launch_bounds__(128) void merge_kernel(MergeArgs a) {
+// One workgroup per (sequence, query head): the split maxima and weights are
+// computed in parallel over splits, then each thread sums one channel over
+// half of the splits with independent loads.
+constexpr int kMergeThreads = 256;
+constexpr int kMaxMergeSplits = 1024;
+
+__device__ __forceinline__ float block_reduce(float v, bool is_max, float* scratch) {
+  v = is_max ? wave_max(v) : wave_sum(v);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  if (lane == 0) scratch[wv] = v;
+  __syncthreads();
+  float r = scratch[0];
+#pragma unroll
+  for (int w = 1; w < kMergeThreads / 64; ++w) r = is_max ? fmaxf(r, scratch[w]) : r + scratch[w];
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
+  __shared__ float wts[kMaxMergeSplits];
+  __shared__ float scratch[kMergeThreads / 64];
+  __shared__ float part[2][kHeadDim];
   const int si = blockIdx.x / a.hq, hq = blockIdx.x % a.hq;
   const MergeSeq& S = a.seq[si];
-  const int c = threadIdx.x;
+  const int tid = threadIdx.x;
   float* o = a.out + ((size_t)S.seq * a.hq + hq) * kHeadDim;
-  if (S.nsplit == 0) { o[c] = 0.f; return; }
+  const int n = S.nsplit;
+  if (n == 0) {
+    if (tid < kHeadDim) o[tid] = 0.f;
+    return;
+  }
   const float* base = a.ws + ((size_t)S.ws_base * a.hq + hq) * kRecFloats;
   const size_t step = (size_t)a.hq * kRecFloats;
-  float M = -__builtin_inff();
-  for (int i = 0; i < S.nsplit; ++i) M = fmaxf(M, base[i * step]);
-  float num = 0.f, den = 0.f;
-  for (int i = 0; i < S.nsplit; ++i) {
-    const float* rec = base + i * step;
-    const float f = __builtin_amdgcn_exp2f(rec[0] - M);
-    num = fmaf(f, rec[4 + c], num);
-    den = fmaf(f, rec[1], den);
+  float mx = -__builtin_inff();
+  for (int i = tid; i < n; i += kMergeThreads) {
+    const float m = base[i * step];
+    wts[i] = m;
+    mx = fmaxf(mx, m);
   }
-  o[c] = num / den;
+  mx = block_reduce(mx, true, scratch);
+  float den = 0.f;
+  for (int i = tid; i < n; i += kMergeThreads) {
+    const float f = __builtin_amdgcn_exp2f(wts[i] - mx);
+    wts[i] = f;
+    den = fmaf(f, base[i * step + 1], den);
+  }
+  den = block_reduce(den, false, scratch);  // also orders the wts writes before the reads below
+  const int c = tid & (kHeadDim - 1), half = tid >> 7;
+  float num = 0.f;
+#pragma unroll 8
+  for (int i = half; i < n; i += 2) num = fmaf(wts[i], base[i * step + 4 + c], num);
+  part[half][c] = num;
+  __syncthreads();
+  if (tid < kHeadDim) o[tid] = (part[0][tid] + part[1][tid]) / den;
 }
 
 template <int BK, int BV, int GQ>
@@ -407,7 +443,7 @@ int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream) {
 
 int launch_merge(const MergeArgs& a, void* stream) {
   if (a.nseq <= 0) return 0;
-  hipLaunchKernelGGL(merge_kernel, dim3(a.nseq * a.hq), dim3(kHeadDim), 0, (hipStream_t)stream, a);
+  hipLaunchKernelGGL(merge_kernel, dim3(a.nseq * a.hq), dim3(kMergeThreads), 0, (hipStream_t)stream, a);
   return (int)hipGetLastError();
 }
 

@@ -478,6 +478,8 @@ kvq_status kvq_set_split_tokens(kvq_cache* c, int32_t tokens) {
   if (tokens < 0 || (tokens > 0 && tokens % c->d.key_group != 0))
     return fail(KVQ_ERR_ARG, "split tokens %d must be 0 or a positive multiple of key_group %d", tokens,
                 c->d.key_group);
+  if (tokens > 0 && (c->cq + tokens - 1) / tokens > kMaxSplits)
+    return fail(KVQ_ERR_ARG, "split tokens %d would give more than %d splits at capacity", tokens, kMaxSplits);
   c->split_tokens = tokens;
   return ok();
 }

@@ -140,7 +140,7 @@ def test_split_setting_and_workspace_bound():
         assert kvq.kvq_workspace_bytes(h) == 32 * (min(512, 131072 // 128) + 1) * rec
         kvq.kvq_set_split_tokens(h, 1024)
         assert kvq.kvq_workspace_bytes(h) == 32 * (128 + 1) * rec
-        for bad in (-32, 33, 100):
+        for bad in (-32, 33, 100, 128):
             with pytest.raises(kvq.KvqError) as e:
                 kvq.kvq_set_split_tokens(h, bad)
             assert e.value.status == kvq.ERR_ARG
