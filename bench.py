@@ -39,9 +39,14 @@ def packed_bytes(L: int, w, bk: int, bv: int) -> int:
     return w.num_kv_heads * (Lq * per_tok + (L - Lq) * w.head_dim * 2 * 2)
 
 
+def matrix_path(w) -> bool:
+    """Whether the library decodes this workload on the matrix cores."""
+    return (w.group_q == 4 and w.bits_k[0] in (1, 2) and w.bits_v[0] in (1, 2) and w.value_group >= 32)
+
+
 def source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("decode.hip", "kvq_internal.h"):
+    for f in ("decode.hip", "decode_mfma.hip", "decode_common.h", "kvq_internal.h", "kvq_layout.h"):
         with open(os.path.join(ROOT, "paper_2607_16248_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -279,7 +284,8 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": f"decode_split_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.group_q}>",
+            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]}>" if matrix_path(w) else
+                       f"decode_split_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.group_q}>"),
             "bytes_per_launch": launch_bytes,
             "kernel_source_sha256_16": source_digest(),
         },

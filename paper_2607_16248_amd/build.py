@@ -24,6 +24,7 @@ COMMON = [f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17",
 SOURCES = [
     ("append.hip", ["-ffp-contract=off"]),
     ("decode.hip", []),
+    ("decode_mfma.hip", []),
     ("dequant.hip", []),
     ("kvq_api.cpp", []),
 ]

@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kvq_internal.h"
+#include "kvq_layout.h"
 
 namespace kvq {
 namespace {
@@ -59,6 +60,38 @@ __device__ __forceinline__ void pack_rows(const uint8_t* codes, int rows, int bi
   }
 }
 
+// Matrix layout (kvq_layout.h), key rows: dword w of a row is plane p = w % b
+// of lane group g = w / b, gathering channels 32*kb + 8*g + e.
+__device__ __forceinline__ void pack_key_rows_matrix(const uint8_t* codes, int rows, int bits, uint8_t* dst) {
+  const int dw_per_row = 4 * bits;
+  for (int k = threadIdx.x; k < rows * dw_per_row; k += blockDim.x) {
+    const int i = k / dw_per_row, w = k % dw_per_row, g = w / bits, p = w % bits;
+    uint32_t v = 0;
+    for (int kb = 0; kb < 4; ++kb)
+      for (int e = 0; e < 8; ++e)
+        v |= (uint32_t)((codes[i * kHeadDim + 32 * kb + 8 * g + e] >> p) & 1u) << pair_bit(kb, e);
+    reinterpret_cast<uint32_t*>(dst + (size_t)i * 16 * bits)[w] = v;
+  }
+}
+
+// Matrix layout, value codes: 32-token blocks of 512*b bytes in MFMA lane order.
+__device__ __forceinline__ void pack_value_blocks_matrix(const uint8_t* codes, int rows, int bits, uint8_t* dst) {
+  const int dw_per_block = 128 * bits;
+  for (int k = threadIdx.x; k < (rows / 32) * dw_per_block; k += blockDim.x) {
+    const int blk = k / dw_per_block, w = k % dw_per_block;
+    const int lane = w / (2 * bits), rem = w % (2 * bits), d = rem / bits, p = rem % bits;
+    const int cl = lane & 15, kg = lane >> 4;
+    uint32_t v = 0;
+    for (int m4 = 0; m4 < 4; ++m4)
+      for (int e = 0; e < 8; ++e) {
+        const int c = 16 * (4 * d + m4) + cl;
+        const int r = e < 4 ? 4 * kg + e : 16 + 4 * kg + (e - 4);
+        v |= (uint32_t)((codes[(blk * 32 + r) * kHeadDim + c] >> p) & 1u) << pair_bit(m4, e);
+      }
+    reinterpret_cast<uint32_t*>(dst + (size_t)blk * 512 * bits)[w] = v;
+  }
+}
+
 __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, int gi, int bk,
                                int bv, uint8_t* codes) {
   uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;
@@ -89,7 +122,10 @@ __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, i
     km[kHeadDim + c] = __builtin_bit_cast(uint16_t, (_Float16)mn);
   }
   __syncthreads();
-  pack_rows(codes, gk, bk, blk + a.kc + (size_t)p0 * 16 * bk);
+  if (a.matrix)
+    pack_key_rows_matrix(codes, gk, bk, blk + a.kc + (size_t)p0 * 16 * bk);
+  else
+    pack_rows(codes, gk, bk, blk + a.kc + (size_t)p0 * 16 * bk);
   __syncthreads();
 
   // values: one item per (token, value group)
@@ -115,10 +151,20 @@ __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, i
       codes[i * kHeadDim + g * a.gv + e] = (ok && sv != 0.0) ? (uint8_t)__builtin_rint((v - mn) / sv) : 0;
     }
     const uint32_t zb = __builtin_bit_cast(uint16_t, (_Float16)mn);
-    reinterpret_cast<uint32_t*>(blk + a.vm)[(size_t)(p0 + i) * ng + g] = (uint32_t)sb | (zb << 16);
+    if (a.matrix) {
+      uint8_t* vmb = blk + a.vm + (size_t)((p0 + i) / 32) * 128 * ng;
+      const int r = (p0 + i) % 32;
+      *reinterpret_cast<uint16_t*>(vmb + value_meta_s(g, r)) = sb;
+      *reinterpret_cast<uint16_t*>(vmb + value_meta_z(g, r, ng)) = (uint16_t)zb;
+    } else {
+      reinterpret_cast<uint32_t*>(blk + a.vm)[(size_t)(p0 + i) * ng + g] = (uint32_t)sb | (zb << 16);
+    }
   }
   __syncthreads();
-  pack_rows(codes, gk, bv, blk + a.vc + (size_t)p0 * 16 * bv);
+  if (a.matrix)
+    pack_value_blocks_matrix(codes, gk, bv, blk + a.vc + (size_t)p0 * 16 * bv);
+  else
+    pack_rows(codes, gk, bv, blk + a.vc + (size_t)p0 * 16 * bv);
 }
 
 // Copy the new tokens that stay fp16 into the ring of head h.

@@ -17,60 +17,13 @@
 //   - wave-wide max and sum use DPP row operations and the row broadcasts.
 #include <hip/hip_runtime.h>
 
+#include "decode_common.h"
 #include "kvq_internal.h"
 
 namespace kvq {
 namespace {
 
-constexpr int kWaves = 4;
-
-__device__ __forceinline__ float h2f(uint32_t bits16) {
-  return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
-}
-
-template <int CTRL, int ROW_MASK = 0xF>
-__device__ __forceinline__ float dpp_mov(float old, float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, old),
-                                                               __builtin_bit_cast(int, v), CTRL,
-                                                               ROW_MASK, 0xF, false));
-}
-
-// DPP controls: quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror,
-// row_mirror, row_bcast:15, row_bcast:31.
-constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kHalfMirror = 0x141, kMirror = 0x140,
-              kBcast15 = 0x142, kBcast31 = 0x143;
-
-__device__ __forceinline__ float readlane63(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-  v += dpp_mov<kQuadXor1>(0.f, v);
-  v += dpp_mov<kQuadXor2>(0.f, v);
-  v += dpp_mov<kHalfMirror>(0.f, v);
-  v += dpp_mov<kMirror>(0.f, v);
-  v += dpp_mov<kBcast15, 0xA>(0.f, v);
-  v += dpp_mov<kBcast31, 0xC>(0.f, v);
-  return readlane63(v);
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-  const float ninf = -__builtin_inff();
-  v = fmaxf(v, dpp_mov<kQuadXor1>(ninf, v));
-  v = fmaxf(v, dpp_mov<kQuadXor2>(ninf, v));
-  v = fmaxf(v, dpp_mov<kHalfMirror>(ninf, v));
-  v = fmaxf(v, dpp_mov<kMirror>(ninf, v));
-  v = fmaxf(v, dpp_mov<kBcast15, 0xA>(ninf, v));
-  v = fmaxf(v, dpp_mov<kBcast31, 0xC>(ninf, v));
-  return readlane63(v);
-}
-
-// LDS written and read back by the same wave: order the accesses.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
+using namespace dec;
 
 // Key row half (64 channels): 8*B bytes = 2*B dwords.
 template <int B>
@@ -94,37 +47,6 @@ __device__ __forceinline__ uint64_t load_value8(const uint8_t* row, int cc) {
   else if constexpr (B == 2) return reinterpret_cast<const uint16_t*>(row)[cc];
   else if constexpr (B == 4) return reinterpret_cast<const uint32_t*>(row)[cc];
   else return reinterpret_cast<const uint64_t*>(row)[cc];
-}
-
-template <int GQ>
-struct QStride {
-  static constexpr int value = GQ <= 4 ? GQ : 8;
-};
-
-template <int GQ>
-struct State {
-  float m[GQ];
-  float l[GQ];
-  float acc[GQ][8];
-};
-
-// Online-softmax update for one pass of 32 tokens held as sig (QK layout:
-// lanes 2t, 2t+1 hold token t).  Writes p to LDS, rescales the state.
-template <int GQ>
-__device__ __forceinline__ void softmax_pass(State<GQ>& st, float (&sig)[GQ], int half, int tl,
-                                             float* p_lds) {
-#pragma unroll
-  for (int g = 0; g < GQ; ++g) {
-    const float mx = wave_max(sig[g]);
-    const float mnew = fmaxf(st.m[g], mx);
-    const float alpha = __builtin_amdgcn_exp2f(st.m[g] - mnew);
-    const float p = __builtin_amdgcn_exp2f(sig[g] - mnew);
-    st.l[g] = st.l[g] * alpha + (half ? 0.f : p);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) st.acc[g][k] *= alpha;
-    st.m[g] = mnew;
-    if (!half) p_lds[tl * GQ + g] = p;
-  }
 }
 
 template <int BK, int BV, int GQ>
@@ -197,149 +119,36 @@ __device__ __forceinline__ void packed_group(const DecodeArgs& a, const uint8_t*
   }
 }
 
-// fp16 tail tokens [Lq, L), read from the ring; pass `pass` covers 32 tokens.
-template <int GQ>
-__device__ __forceinline__ void tail_pass(const DecodeArgs& a, const DecodeSeq& S, const uint8_t* blk,
-                                          int pass, const float* qp, float* p_lds, State<GQ>& st,
-                                          int lane) {
-  constexpr int QS = QStride<GQ>::value;
-  const int ntail = S.L - S.Lq;
-  const int tl = lane >> 1, half = lane & 1;
-  const int idx = pass * 32 + tl;
-  float sig[GQ];
-#pragma unroll
-  for (int g = 0; g < GQ; ++g) sig[g] = 0.f;
-  if (idx < ntail) {
-    const int slot = (S.Lq + idx) % a.W;
-    const uint4* kr = reinterpret_cast<const uint4*>(blk + a.tk + ((size_t)slot * kHeadDim + half * 64) * 2);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const uint4 v = kr[i];
-      const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x = h2f((w4[e >> 1] >> ((e & 1) * 16)) & 0xFFFF);
-        const float* qv = qp + (half * 64 + i * 8 + e) * QS;
-#pragma unroll
-        for (int g = 0; g < GQ; ++g) sig[g] = fmaf(qv[g], x, sig[g]);
-      }
-    }
-  }
-#pragma unroll
-  for (int g = 0; g < GQ; ++g) {
-    sig[g] += dpp_mov<kQuadXor1>(0.f, sig[g]);
-    if (idx >= ntail) sig[g] = -__builtin_inff();
-  }
-  softmax_pass<GQ>(st, sig, half, tl, p_lds);
-  wave_lds_sync();
-  const int tq = lane >> 4, cc = lane & 15;
-  for (int tt = tq; tt < 32; tt += 4) {
-    const int i2 = pass * 32 + tt;
-    if (i2 >= ntail) break;
-    const int slot = (S.Lq + i2) % a.W;
-    const uint4 v = *reinterpret_cast<const uint4*>(blk + a.tv + ((size_t)slot * kHeadDim + cc * 8) * 2);
-    const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
-    const float* pp = p_lds + tt * GQ;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const float x = h2f((w4[k >> 1] >> ((k & 1) * 16)) & 0xFFFF);
-#pragma unroll
-      for (int g = 0; g < GQ; ++g) st.acc[g][k] = fmaf(pp[g], x, st.acc[g][k]);
-    }
-  }
-  wave_lds_sync();
-}
-
 template <int BK, int BV, int GQ>
 __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   constexpr int QS = QStride<GQ>::value;
   __shared__ float qp_lds[kWaves][kHeadDim * QS];
   __shared__ float p_lds[kWaves][32 * GQ];
-  __shared__ float red_m[kWaves][GQ], red_l[kWaves][GQ];
-  __shared__ float red_acc[kWaves][GQ * kHeadDim];
+  __shared__ Reduce<GQ> red;
 
-  const int wg = blockIdx.x;
-  int si = 0;
-  for (int i = 1; i < a.nseq; ++i) si = (a.seq[i].wg_begin <= wg) ? i : si;
-  const DecodeSeq& S = a.seq[si];
-  const int local = wg - S.wg_begin;
-  const int h = local / S.nsplit, sp = local % S.nsplit;
-  const uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;
+  const Work wk = find_work(a);
+  const DecodeSeq& S = a.seq[wk.si];
+  const uint8_t* blk = a.arena + S.head0 + (uint64_t)wk.h * a.head_stride;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
 
-  // this lane's two channels of the GQ query heads, pre-scaled to base 2
-  const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)h * GQ) * kHeadDim;
   float qs0[GQ], qs1[GQ];
-#pragma unroll
-  for (int g = 0; g < GQ; ++g) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(qrow + g * kHeadDim)[lane];
-    qs0[g] = h2f(w & 0xFFFF) * a.qscale;
-    qs1[g] = h2f(w >> 16) * a.qscale;
-  }
-
+  load_q_scaled<GQ>(a, S, wk.h, lane, qs0, qs1);
   State<GQ> st;
-#pragma unroll
-  for (int g = 0; g < GQ; ++g) {
-    st.m[g] = -__builtin_inff();
-    st.l[g] = 0.f;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) st.acc[g][k] = 0.f;
-  }
+  init_state<GQ>(st);
 
   float* qp = qp_lds[wv];
   float* pl = p_lds[wv];
-  if (sp < S.nq) {
-    const int t0 = sp * a.split_tokens;
+  if (wk.sp < S.nq) {
+    const int t0 = wk.sp * a.split_tokens;
     const int t1 = min(S.Lq, t0 + a.split_tokens);
     for (int j = t0 / a.gk + wv; j < t1 / a.gk; j += kWaves)
       packed_group<BK, BV, GQ>(a, blk, j, qs0, qs1, qp, pl, st, lane);
   } else {
-#pragma unroll
-    for (int g = 0; g < GQ; ++g) {
-      qp[(2 * lane) * QS + g] = qs0[g];
-      qp[(2 * lane + 1) * QS + g] = qs1[g];
-    }
-    wave_lds_sync();
-    for (int pass = wv; pass * 32 < S.L - S.Lq; pass += kWaves) tail_pass<GQ>(a, S, blk, pass, qp, pl, st, lane);
+    tail_split<GQ>(a, S, blk, qs0, qs1, qp, pl, st, lane, wv);
   }
-
-  // combine: lanes of a wave, then the waves of the workgroup
-#pragma unroll
-  for (int g = 0; g < GQ; ++g) {
-    st.l[g] = wave_sum(st.l[g]);
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      st.acc[g][k] += __shfl_xor(st.acc[g][k], 16);
-      st.acc[g][k] += __shfl_xor(st.acc[g][k], 32);
-    }
-  }
-  if (lane < 16) {
-#pragma unroll
-    for (int g = 0; g < GQ; ++g)
-#pragma unroll
-      for (int k = 0; k < 8; ++k) red_acc[wv][g * kHeadDim + lane * 8 + k] = st.acc[g][k];
-  }
-  if (lane == 0) {
-#pragma unroll
-    for (int g = 0; g < GQ; ++g) { red_m[wv][g] = st.m[g]; red_l[wv][g] = st.l[g]; }
-  }
+  stage_state<GQ>(st, red, lane, wv);
   __syncthreads();
-  for (int idx = threadIdx.x; idx < GQ * kHeadDim; idx += blockDim.x) {
-    const int g = idx / kHeadDim, c = idx % kHeadDim;
-    float M = -__builtin_inff();
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red_m[w][g]);
-    float val = 0.f, lsum = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float f = __builtin_amdgcn_exp2f(red_m[w][g] - M);
-      val = fmaf(f, red_acc[w][idx], val);
-      lsum = fmaf(f, red_l[w][g], lsum);
-    }
-    float* rec = a.ws + ((size_t)(S.ws_base + sp) * a.hq + (size_t)h * GQ + g) * kRecFloats;
-    rec[4 + c] = val;
-    if (c == 0) { rec[0] = M; rec[1] = lsum; }
-  }
+  write_record<GQ>(a, S, wk.h, wk.sp, red);
 }
 
 // One workgroup per (sequence, query head): the split maxima and weights are

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kvq_internal.h"
+#include "kvq_layout.h"
 
 namespace kvq {
 namespace {
@@ -18,6 +19,25 @@ __device__ __forceinline__ uint32_t code_at(const uint8_t* row, int c, int bits)
   return ((uint32_t)row[bit >> 3] >> (bit & 7)) & ((1u << bits) - 1u);
 }
 
+// Code of channel c from a matrix-layout key row / value block.
+__device__ __forceinline__ uint32_t key_code_matrix(const uint8_t* row, int c, int bits) {
+  uint32_t code = 0;
+  for (int p = 0; p < bits; ++p) {
+    const BitLoc b = key_bit(c, p, bits);
+    code |= ((reinterpret_cast<const uint32_t*>(row)[b.word] >> b.bit) & 1u) << p;
+  }
+  return code;
+}
+
+__device__ __forceinline__ uint32_t value_code_matrix(const uint8_t* block, int r, int c, int bits) {
+  uint32_t code = 0;
+  for (int p = 0; p < bits; ++p) {
+    const BitLoc b = value_bit(r, c, p, bits);
+    code |= ((reinterpret_cast<const uint32_t*>(block)[b.word] >> b.bit) & 1u) << p;
+  }
+  return code;
+}
+
 __global__ __launch_bounds__(128) void dequant_kernel(DequantArgs a) {
   const int ti = blockIdx.x / a.hkv, h = blockIdx.x % a.hkv;
   const int p = a.tok0 + ti, c = threadIdx.x;
@@ -25,10 +45,21 @@ __global__ __launch_bounds__(128) void dequant_kernel(DequantArgs a) {
   float kv, vv;
   if (p < a.Lq) {
     const uint16_t* km = reinterpret_cast<const uint16_t*>(blk + a.km) + (size_t)(p / a.gk) * 2 * kHeadDim;
-    kv = fmaf((float)code_at(blk + a.kc + (size_t)p * 16 * a.bk, c, a.bk), h2f(km[c]), h2f(km[kHeadDim + c]));
-    const int ng = kHeadDim / a.gv;
-    const uint32_t meta = reinterpret_cast<const uint32_t*>(blk + a.vm)[(size_t)p * ng + c / a.gv];
-    vv = fmaf((float)code_at(blk + a.vc + (size_t)p * 16 * a.bv, c, a.bv), h2f(meta & 0xFFFF), h2f(meta >> 16));
+    const uint8_t* krow = blk + a.kc + (size_t)p * 16 * a.bk;
+    const uint32_t kcode = a.matrix ? key_code_matrix(krow, c, a.bk) : code_at(krow, c, a.bk);
+    kv = fmaf((float)kcode, h2f(km[c]), h2f(km[kHeadDim + c]));
+    const int ng = kHeadDim / a.gv, g = c / a.gv;
+    if (a.matrix) {
+      const uint8_t* vblk = blk + a.vc + (size_t)(p / 32) * 512 * a.bv;
+      const uint8_t* vmb = blk + a.vm + (size_t)(p / 32) * 128 * ng;
+      const int r = p % 32;
+      const uint32_t vcode = value_code_matrix(vblk, r, c, a.bv);
+      vv = fmaf((float)vcode, h2f(*reinterpret_cast<const uint16_t*>(vmb + value_meta_s(g, r))),
+                h2f(*reinterpret_cast<const uint16_t*>(vmb + value_meta_z(g, r, ng))));
+    } else {
+      const uint32_t meta = reinterpret_cast<const uint32_t*>(blk + a.vm)[(size_t)p * ng + g];
+      vv = fmaf((float)code_at(blk + a.vc + (size_t)p * 16 * a.bv, c, a.bv), h2f(meta & 0xFFFF), h2f(meta >> 16));
+    }
   } else {
     const size_t slot = (size_t)(p % a.W) * kHeadDim + c;
     kv = h2f(reinterpret_cast<const uint16_t*>(blk + a.tk)[slot]);
@@ -39,7 +70,45 @@ __global__ __launch_bounds__(128) void dequant_kernel(DequantArgs a) {
   a.V_out[o] = vv;
 }
 
+// One workgroup per 32-token block: codes into LDS, then canonical rows.
+__global__ __launch_bounds__(256) void export_kernel(ExportArgs a) {
+  __shared__ uint8_t kc[32 * kHeadDim], vc[32 * kHeadDim];
+  const int b = blockIdx.x;
+  const int ng = kHeadDim / a.gv;
+  for (int idx = threadIdx.x; idx < 32 * kHeadDim; idx += blockDim.x) {
+    const int r = idx / kHeadDim, c = idx % kHeadDim;
+    kc[idx] = (uint8_t)key_code_matrix(a.blk + a.kc + (size_t)(32 * b + r) * 16 * a.bk, c, a.bk);
+    vc[idx] = (uint8_t)value_code_matrix(a.blk + a.vc + (size_t)b * 512 * a.bv, r, c, a.bv);
+  }
+  __syncthreads();
+  for (int k = threadIdx.x; k < 32 * 4 * a.bk; k += blockDim.x) {
+    const int i = k / (4 * a.bk), w = k % (4 * a.bk), per = 32 / a.bk;
+    uint32_t v = 0;
+    for (int e = 0; e < per; ++e) v |= (uint32_t)kc[i * kHeadDim + w * per + e] << (e * a.bk);
+    reinterpret_cast<uint32_t*>(a.kc_out + (size_t)(32 * b + i) * 16 * a.bk)[w] = v;
+  }
+  for (int k = threadIdx.x; k < 32 * 4 * a.bv; k += blockDim.x) {
+    const int i = k / (4 * a.bv), w = k % (4 * a.bv), per = 32 / a.bv;
+    uint32_t v = 0;
+    for (int e = 0; e < per; ++e) v |= (uint32_t)vc[i * kHeadDim + w * per + e] << (e * a.bv);
+    reinterpret_cast<uint32_t*>(a.vc_out + (size_t)(32 * b + i) * 16 * a.bv)[w] = v;
+  }
+  const uint8_t* vmb = a.blk + a.vm + (size_t)b * 128 * ng;
+  for (int k = threadIdx.x; k < 32 * ng; k += blockDim.x) {
+    const int r = k / ng, g = k % ng;
+    const uint32_t sv = *reinterpret_cast<const uint16_t*>(vmb + value_meta_s(g, r));
+    const uint32_t zv = *reinterpret_cast<const uint16_t*>(vmb + value_meta_z(g, r, ng));
+    reinterpret_cast<uint32_t*>(a.vm_out)[(size_t)(32 * b + r) * ng + g] = sv | (zv << 16);
+  }
+}
+
 }  // namespace
+
+int launch_export(const ExportArgs& a, void* stream) {
+  if (a.nblocks <= 0) return 0;
+  hipLaunchKernelGGL(export_kernel, dim3(a.nblocks), dim3(256), 0, (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
 
 int launch_dequant(const DequantArgs& a, void* stream) {
   if (a.ntok <= 0) return 0;

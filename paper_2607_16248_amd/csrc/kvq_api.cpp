@@ -31,6 +31,7 @@ struct kvq_cache {
   std::vector<uint64_t> head0;
   std::vector<HeadLayout> lay;
   std::vector<int32_t> L, Lq;
+  std::vector<uint8_t> matrix;  // 1: matrix layout and the matrix-core decode kernel
   int32_t split_tokens = 0;
 };
 
@@ -40,7 +41,22 @@ thread_local std::string g_err;
 
 constexpr int kMaxSplits = 512;          // packed splits per sequence and kv head
 constexpr int kMinGroupsPerSplit = 4;    // one key group per wave at least
-constexpr int kTargetWorkgroups = 2048;  // about 8 per compute unit
+constexpr int kWorkgroupsPerCU = 2;      // resident decode workgroups per compute unit
+
+// Decode workgroups that fit the current device at once (one round of the grid).
+int64_t target_workgroups() {
+  static thread_local int cached_dev = -1;
+  static thread_local int64_t cached = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 512;
+  if (dev != cached_dev) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    cached_dev = dev;
+    cached = (int64_t)cus * kWorkgroupsPerCU;
+  }
+  return cached;
+}
 
 kvq_status fail(kvq_status s, const char* fmt, ...) {
   char buf[512];
@@ -110,7 +126,8 @@ int32_t split_tokens_for(const kvq_cache* c) {
     total += (int64_t)c->Lq[i] * c->d.num_kv_heads;
     lq_max = std::max<int64_t>(lq_max, c->Lq[i]);
   }
-  int64_t st = (total + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  const int64_t target = target_workgroups();
+  int64_t st = (total + target - 1) / target;
   st = std::max<int64_t>(st, (lq_max + kMaxSplits - 1) / kMaxSplits);
   st = (st + gk - 1) / gk * gk;
   st = std::max<int64_t>(st, (int64_t)gk * kMinGroupsPerSplit);
@@ -187,6 +204,9 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   }
   c->L.assign(d->batch, 0);
   c->Lq.assign(d->batch, 0);
+  for (int i = 0; i < d->batch; ++i)
+    c->matrix.push_back(kvq::matrix_decode_supported(c->bk[i], c->bv[i], d->num_q_heads / d->num_kv_heads,
+                                                     d->value_group) ? 1 : 0);
   *out = c;
   return ok();
 }
@@ -251,6 +271,7 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int32_t n_max,
       a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
       a.n_max = n_max; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
       a.quantize = quant ? 1 : 0;
+      a.matrix = c->matrix[cls.second[0]];
       int wg = 0, n = 0;
       for (int i : cls.second) {
         kvq::AppendSeq& s = a.seq[n++];
@@ -339,7 +360,9 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     }
     a.nseq = n;
     a.total_wg = wg;
-    const int e = kvq::launch_decode(a, cls.first.first, cls.first.second, d.num_q_heads / d.num_kv_heads, stream);
+    const int e = c->matrix[cls.second[0]]
+                      ? kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, stream)
+                      : kvq::launch_decode(a, cls.first.first, cls.first.second, d.num_q_heads / d.num_kv_heads, stream);
     if (e) return hip_fail(e, "decode launch");
   }
   return KVQ_OK;
@@ -409,6 +432,7 @@ kvq_status kvq_dequant(const kvq_cache* c, int32_t seq, int32_t tok0, int32_t nt
   a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
   a.hkv = c->d.num_kv_heads; a.gk = c->d.key_group; a.gv = c->d.value_group; a.W = c->W;
   a.bk = c->bk[seq]; a.bv = c->bv[seq]; a.Lq = c->Lq[seq]; a.tok0 = tok0; a.ntok = ntok;
+  a.matrix = c->matrix[seq];
   const int e = kvq::launch_dequant(a, stream);
   if (e) return hip_fail(e, "dequant launch");
   return ok();
@@ -438,11 +462,29 @@ kvq_status kvq_export(const kvq_cache* c, int32_t seq, int32_t h, void* dst, siz
                              {lay.vc, Lq * 16 * c->bv[seq]},
                              {lay.vm, Lq * (D / c->d.value_group) * 4}};
   hipStream_t s = static_cast<hipStream_t>(stream);
-  for (auto& p : part) {
-    if (p[1] == 0) continue;
-    const hipError_t e = hipMemcpyAsync(o, blk + p[0], p[1], hipMemcpyDeviceToDevice, s);
-    if (e != hipSuccess) return hip_fail(e, "export copy");
-    o += p[1];
+  if (c->matrix[seq]) {
+    // key meta is stored canonically; codes and value meta are re-ordered by a kernel
+    if (part[1][1]) {
+      const hipError_t e = hipMemcpyAsync(o + part[0][1], blk + part[1][0], part[1][1], hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return hip_fail(e, "export copy");
+    }
+    kvq::ExportArgs x{};
+    x.blk = blk;
+    x.kc_out = o;
+    x.vc_out = o + part[0][1] + part[1][1];
+    x.vm_out = x.vc_out + part[2][1];
+    x.kc = (uint32_t)lay.kc; x.vc = (uint32_t)lay.vc; x.vm = (uint32_t)lay.vm;
+    x.bk = c->bk[seq]; x.bv = c->bv[seq]; x.gv = c->d.value_group; x.nblocks = (int32_t)(Lq / 32);
+    const int e = kvq::launch_export(x, stream);
+    if (e) return hip_fail(e, "export launch");
+    o += part[0][1] + part[1][1] + part[2][1] + part[3][1];
+  } else {
+    for (auto& p : part) {
+      if (p[1] == 0) continue;
+      const hipError_t e = hipMemcpyAsync(o, blk + p[0], p[1], hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return hip_fail(e, "export copy");
+      o += p[1];
+    }
   }
   const size_t W = c->W, n = L - Lq, first = Lq % W;
   for (uint64_t ring : {lay.tk, lay.tv}) {

@@ -67,6 +67,7 @@ struct AppendArgs {
   uint32_t kc, km, vc, vm, tk, tv;
   int32_t n_max, hkv, gk, gv, W, nseq, total_wg;
   int32_t quantize;   // 1: pack groups in this launch
+  int32_t matrix;     // 1: matrix layout (kvq_layout.h) for this bit class
   AppendSeq seq[kMaxSeqPerLaunch];
 };
 
@@ -114,11 +115,28 @@ struct DequantArgs {
   uint64_t head_stride;
   uint32_t kc, km, vc, vm, tk, tv;
   int32_t hkv, gk, gv, W, bk, bv, Lq, tok0, ntok;
+  int32_t matrix;
+};
+
+// ---------------------------------------------------------------- export
+
+// Matrix-layout codes and value meta of one (seq, head) rewritten in the
+// canonical order: 32-token blocks [0, Lq / 32).
+struct ExportArgs {
+  const uint8_t* blk;   // (seq, head) block
+  uint8_t* kc_out;      // canonical key codes [Lq][16*bk]
+  uint8_t* vc_out;      // canonical value codes [Lq][16*bv]
+  uint8_t* vm_out;      // canonical value meta [Lq][128/gv][2] fp16
+  uint32_t kc, vc, vm;
+  int32_t bk, bv, gv, nblocks;
 };
 
 // Launchers (defined next to their kernels).  Return a hipError_t as int.
 int launch_append(const AppendArgs& a, int bk, int bv, void* stream);
 int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
+int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, void* stream);
+bool matrix_decode_supported(int bk, int bv, int gq, int gv);
+int launch_export(const ExportArgs& a, void* stream);
 int launch_merge(const MergeArgs& a, void* stream);
 int launch_dequant(const DequantArgs& a, void* stream);
 int launch_fill_zero(void* dst, size_t words, void* stream);
