@@ -23,8 +23,13 @@
 //     holds p for the 8 tokens its B fragment needs (no transpose); output
 //     columns whose group differs from the channel's are discarded.
 //
-// Packed bits become operands with one AND and one 24-bit multiply per
-// element pair; the layouts that make this possible are in kvq_layout.h.
+// Packed bits become operands with one AND per element pair: a set bit at
+// mantissa position w of a half is the exact fp16 subnormal 2^(w - 24).
+// The key-side weights 2^w depend only on the channel and are folded into
+// q~ once per decode; the value-side weights are split into a per-token-pair
+// part folded into the value scales and a per-channel-block part applied to
+// the accumulators at the end; the common 2^-24 goes into the fp32 scales.
+// The layouts that place the bits are in kvq_layout.h.
 #include <hip/hip_runtime.h>
 
 #include "decode_common.h"
@@ -47,20 +52,34 @@ constexpr int kQRow = 80;  // dwords per Q' row in LDS: 64 + 16 of padding again
 __device__ __forceinline__ h2_t u2h(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
 __device__ __forceinline__ uint32_t h2u(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
 
-// One MFMA operand (8 halves) from the bits of 4-channel-block blk4 in x:
-// element pair i sits at bits (s, s + 16) with s = pair_bit(blk4, 2i); a set
-// bit becomes the fp16 value whose bit pattern is `one` (1.0 or 2.0).
-__device__ __forceinline__ h8_t unpack8(uint32_t x, int blk4, uint32_t one) {
-  const uint32_t src = blk4 < 2 ? x : x >> 8;
-  const int base = 4 * (blk4 & 1);
+// One MFMA operand (8 halves) from the bits of 4-channel block blk4 in x
+// (bit plane `plane`): element pair i sits at bits (s, s + 16) with
+// s = pair_bit(blk4, 2i), and a single AND leaves each half equal to
+// bit * 2^(w - 24), an exact fp16 subnormal, with weight
+// w = 4*(blk4 & 1) + i + plane.  The other operand or the output carries
+// the inverse weight, so no multiply per element is needed.
+__device__ __forceinline__ h8_t unpack8(uint32_t x, int blk4, int plane) {
+  const uint32_t src = blk4 < 2 ? (plane ? x << 1 : x) : (plane ? x >> 7 : x >> 8);
+  const int base = 4 * (blk4 & 1) + plane;
   u4_t w;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = __umul24(src & (0x10001u << (base + i)), one >> (base + i));
+  for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (base + i));
   return __builtin_bit_cast(h8_t, w);
 }
 
 __device__ __forceinline__ f4_t mfma(h8_t a, h8_t b, f4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// Maximum over the four lane rows (lanes l, l^16, l^32, l^48) with the
+// gfx950 row-swap permutes.
+__device__ __forceinline__ float max_across_rows(float v) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, v);
+  const auto s32 = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  v = fmaxf(__builtin_bit_cast(float, (uint32_t)s32[0]), __builtin_bit_cast(float, (uint32_t)s32[1]));
+  const uint32_t w = __builtin_bit_cast(uint32_t, v);
+  const auto s16 = __builtin_amdgcn_permlane16_swap(w, w, false, false);
+  return fmaxf(__builtin_bit_cast(float, (uint32_t)s16[0]), __builtin_bit_cast(float, (uint32_t)s16[1]));
 }
 
 __device__ __forceinline__ float pick4(const float (&v)[kGQ], int i) {
@@ -71,7 +90,7 @@ __device__ __forceinline__ float pick4(const float (&v)[kGQ], int i) {
 template <int BK, int BV>
 struct BlockData {
   uint32_t s;          // key scales of channels 2*lane, 2*lane+1 (this block's key group)
-  h8_t az[4];          // key zero-points in A-operand order
+  uint32_t z;          // key zero-points of the same channels
   uint32_t kx[2][BK];  // key codes of tokens 16*mb + (lane & 15)
   uint32_t vx[2 * BV]; // value codes of this lane
   uint2 s01, s23, z01, z23;  // value scales / zeros of this lane's tokens and group
@@ -83,9 +102,7 @@ __device__ __forceinline__ void load_block(const DecodeArgs& a, const uint8_t* b
   const int col = lane & 15, row = lane >> 4;
   const uint8_t* kmeta = blk + a.km + (size_t)j * 2 * kHeadDim * 2;
   o.s = reinterpret_cast<const uint32_t*>(kmeta)[lane];
-  const h8_t* zp = reinterpret_cast<const h8_t*>(kmeta + kHeadDim * 2);
-#pragma unroll
-  for (int kb = 0; kb < 4; ++kb) o.az[kb] = zp[4 * kb + row];
+  o.z = reinterpret_cast<const uint32_t*>(kmeta + kHeadDim * 2)[lane];
   const int tok = j * a.gk + sub * 32;
 #pragma unroll
   for (int mb = 0; mb < 2; ++mb) {
@@ -117,8 +134,8 @@ __device__ __forceinline__ void load_block(const DecodeArgs& a, const uint8_t* b
 }
 
 template <int BK, int BV>
-__global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
-  __shared__ uint32_t q_lds[kWaves][2 * kGQ * kQRow];
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void decode_mfma_kernel(DecodeArgs a) {
+  __shared__ uint32_t q_lds[kWaves][(2 * kGQ + 1) * kQRow];  // Q' hi rows, lo rows, key zero-points
   __shared__ float qp_lds[kWaves][kHeadDim * kGQ];  // fp16 tail split only
   __shared__ float p_lds[kWaves][32 * kGQ];         // fp16 tail split only
   __shared__ Reduce<kGQ> red;
@@ -126,7 +143,8 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
   const Work wk = find_work(a);
   const DecodeSeq& S = a.seq[wk.si];
   const uint8_t* blk = a.arena + S.head0 + (uint64_t)wk.h * a.head_stride;
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  // wave index as a scalar so that per-wave loop bounds stay in SGPRs
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
   if (wk.sp >= S.nq) {  // fp16 tail tokens: vector path
     float qs0[kGQ], qs1[kGQ];
@@ -145,7 +163,10 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
   const int ng = kHeadDim / a.gv, gsel = xc & (ng - 1);
   const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * kGQ) * kHeadDim;
 
-  // q~ = q * 2^-e per head with max |q~| < 1
+  // q~ = q * 2^-e per head with max |q~| < 1.  For the code MFMA each lane's
+  // channel pair (2*lane, 2*lane+1) also carries 2^-w, w = the bit weight of
+  // those channels in the unpacked key operand.
+  const float wq = ldexpf(1.f, -(4 * ((lane >> 4) & 1) + (lane & 3)));
   uint32_t qt[kGQ];
   float inv[kGQ], csc[kGQ];
 #pragma unroll
@@ -156,10 +177,10 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     int e = 0;
     frexpf(mx, &e);
     inv[g] = ldexpf(1.f, -e);
-    csc[g] = ldexpf(a.qscale, e);
+    csc[g] = ldexpf(a.qscale, e + 24);  // undoes 2^-e and the 2^-24 of the code operand
     h2_t t;
-    t.x = (_Float16)(q0 * inv[g]);
-    t.y = (_Float16)(q1 * inv[g]);
+    t.x = (_Float16)(q0 * inv[g] * wq);
+    t.y = (_Float16)(q1 * inv[g] * wq);
     qt[g] = h2u(t);
   }
   const float cs = pick4(csc, hc);
@@ -184,7 +205,6 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
   const int t0 = wk.sp * a.split_tokens;
   const int t1 = min(S.Lq, t0 + a.split_tokens);
   uint32_t* ql = q_lds[wv];
-  constexpr uint32_t kOne = 0x3C00u, kTwo = 0x4000u;
 
   // This wave's 32-token blocks: key groups j0 + wv + kWaves*n, each of
   // gk/32 blocks.  Loads run one block ahead of the arithmetic.
@@ -193,18 +213,12 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
   const int ngroups = j0 < jend ? (jend - j0 + kWaves - 1) / kWaves : 0;
   const int nblocks = ngroups * bpg;
 
-  BlockData<BK, BV> cur, nxt;
-  if (nblocks > 0) load_block<BK, BV>(a, blk, j0, 0, lane, gsel, ng, cur);
   f4_t dz = {0.f, 0.f, 0.f, 0.f};
   h8_t bp[4];
-  for (int i = 0; i < nblocks; ++i) {
-    const int n = i / bpg, sub = i - n * bpg;
-    if (i + 1 < nblocks) {
-      const int n1 = (i + 1) / bpg;
-      load_block<BK, BV>(a, blk, j0 + kWaves * n1, (i + 1) - n1 * bpg, lane, gsel, ng, nxt);
-    }
-    if (sub == 0) {
-      // Q' = q~ (.) s of key group j, hi and lo halves, through LDS
+  auto process = [&](const BlockData<BK, BV>& cur, int i) {
+    if (i % bpg == 0) {
+      // Q' = q~ (.) s of the block's key group, hi and lo halves, and the
+      // group's zero-points, re-laid out through LDS
       wave_lds_sync();
 #pragma unroll
       for (int g = 0; g < kGQ; ++g) {
@@ -214,13 +228,18 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
         ql[g * kQRow + lane] = h2u(hi);
         ql[(kGQ + g) * kQRow + lane] = h2u(lo);
       }
+      ql[2 * kGQ * kQRow + lane] = cur.z;
       wave_lds_sync();
+      h8_t az[4];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+      for (int kb = 0; kb < 4; ++kb) {
         bp[kb] = *reinterpret_cast<const h8_t*>(&ql[(part * kGQ + hc) * kQRow + 16 * kb + 4 * row]);
+        az[kb] = *reinterpret_cast<const h8_t*>(&ql[2 * kGQ * kQRow + 16 * kb + 4 * row]);
+      }
       dz = (f4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) dz = mfma(cur.az[kb], bq[kb], dz);
+      for (int kb = 0; kb < 4; ++kb) dz = mfma(az[kb], bq[kb], dz);
+      dz *= 0x1p-24f;  // to the scale of the code products
     }
 
     // scores of tokens 16*mb + 4*row + e of the block, e < 4
@@ -231,7 +250,7 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int p = 0; p < BK; ++p) d[mb] = mfma(unpack8(cur.kx[mb][p], kb, p ? kTwo : kOne), bp[kb], d[mb]);
+        for (int p = 0; p < BK; ++p) d[mb] = mfma(unpack8(cur.kx[mb][p], kb, p), bp[kb], d[mb]);
     }
     float sc[8];
 #pragma unroll
@@ -246,8 +265,7 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     float bm = sc[0];
 #pragma unroll
     for (int t = 1; t < 8; ++t) bm = fmaxf(bm, sc[t]);
-    bm = fmaxf(bm, __shfl_xor(bm, 16));
-    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    bm = max_across_rows(bm);
     const float mnew = fmaxf(m, bm);
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
@@ -273,7 +291,8 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
       const h2_t ph = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(p[2 * t], p[2 * t + 1]));
       const h2_t pl = __builtin_bit_cast(
           h2_t, __builtin_amdgcn_cvt_pkrtz(p[2 * t] - (float)ph.x, p[2 * t + 1] - (float)ph.y));
-      const h2_t s2 = u2h(sv[t]);
+      // value scale times 2^-t, the inverse of the pair's bit weight
+      const h2_t s2 = t == 0 ? u2h(sv[t]) : u2h(sv[t]) * (h2_t){(_Float16)(1.f / (1 << t)), (_Float16)(1.f / (1 << t))};
       const h2_t hi = ph * s2;
       const h2_t lo = __builtin_elementwise_fma(pl, s2, __builtin_elementwise_fma(ph, s2, -hi));
       bhi[t] = h2u(hi);
@@ -286,12 +305,36 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
     for (int mb = 0; mb < 8; ++mb) {
 #pragma unroll
       for (int p2 = 0; p2 < BV; ++p2) {
-        const h8_t av = unpack8(cur.vx[(mb >> 2) * BV + p2], mb & 3, p2 ? kTwo : kOne);
+        const h8_t av = unpack8(cur.vx[(mb >> 2) * BV + p2], mb & 3, p2);
         acc[mb] = mfma(av, BH, acc[mb]);
         acc[mb] = mfma(av, BL, acc[mb]);
       }
     }
-    cur = nxt;
+  };
+  // block i of this wave: key group j0 + kWaves*(i / bpg), 32-token part i % bpg
+  auto load = [&](int i, BlockData<BK, BV>& o) {
+    load_block<BK, BV>(a, blk, j0 + kWaves * (i / bpg), i % bpg, lane, gsel, ng, o);
+  };
+
+  // Three buffers, loads two blocks ahead of the arithmetic.  The loads are
+  // unconditional (past the end they re-read the last block) so every path
+  // through the loop has the same loads in flight and the memory waits stay
+  // exact.
+  if (nblocks > 0) {
+    const int last = nblocks - 1;
+    BlockData<BK, BV> b0, b1, b2;
+    load(0, b0);
+    load(min(1, last), b1);
+    for (int i = 0; i < nblocks; i += 3) {
+      load(min(i + 2, last), b2);
+      process(b0, i);
+      if (i + 1 >= nblocks) break;
+      load(min(i + 3, last), b0);
+      process(b1, i + 1);
+      if (i + 2 >= nblocks) break;
+      load(min(i + 4, last), b1);
+      process(b2, i + 2);
+    }
   }
 
   // sums over the lane rows; the lanes of one head agree on m and l
@@ -303,7 +346,8 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(DecodeArgs a) {
   for (int mb = 0; mb < 8; ++mb) {
     if (xc == (16 * mb) / a.gv) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) red.acc[wv][hc * kHeadDim + 16 * mb + 4 * row + e] = acc[mb][e] + zacc;
+      for (int e = 0; e < 4; ++e)  // undo the channel block's bit weight 2^(4*(mb & 1)) and the 2^-24
+        red.acc[wv][hc * kHeadDim + 16 * mb + 4 * row + e] = fmaf(acc[mb][e], (mb & 1) ? 0x1p20f : 0x1p24f, zacc);
     }
   }
   if (row == 0 && xc == 0) {
