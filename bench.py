@@ -117,6 +117,8 @@ def main():
     ap.add_argument("--kernel-iters", type=int, default=256)
     ap.add_argument("--cpu-heads", type=int, default=4, help="kv heads in the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="end with 4 plain device copies of 256 MiB (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -290,6 +292,13 @@ def main():
             "kernel_source_sha256_16": source_digest(),
         },
     }
+    if args.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.uint8, device=dev).fill_(3)
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         log("[bench] CPU baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_heads, w.num_kv_heads))
