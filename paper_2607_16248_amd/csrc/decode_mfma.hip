@@ -86,6 +86,27 @@ __device__ __forceinline__ float pick4(const float (&v)[kGQ], int i) {
   return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
 }
 
+// Buffer resource over one (sequence, kv head) block.  Every load is
+// base + per-lane offset + uniform offset: the per-block part is scalar
+// arithmetic and the vector ALU does no address math.  The host keeps the
+// block under 4 GiB for this kernel.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t head_rsrc(const uint8_t* base, uint64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, (int)(uint32_t)bytes,
+                                           0x00020000);
+}
+
+__device__ __forceinline__ uint32_t ld32(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t s) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, v, s, 0);
+}
+__device__ __forceinline__ uint2 ld64(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t s) {
+  typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+  const u2 x = __builtin_amdgcn_raw_buffer_load_b64(r, v, s, 0);
+  return make_uint2(x[0], x[1]);
+}
+__device__ __forceinline__ u4_t ld128(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t s) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 0);
+}
+
 // Everything one 32-token block reads from memory.
 template <int BK, int BV>
 struct BlockData {
@@ -93,47 +114,49 @@ struct BlockData {
   uint32_t z;          // key zero-points of the same channels
   uint32_t kx[2][BK];  // key codes of tokens 16*mb + (lane & 15)
   uint32_t vx[2 * BV]; // value codes of this lane
-  uint2 s01, s23, z01, z23;  // value scales / zeros of this lane's tokens and group
+  u4_t sv, zv;         // value scales / zeros of this lane's 8 tokens and group, element order
+};
+
+// Per-lane byte offsets of one block's loads (the per-block parts are scalar).
+struct LaneOffsets {
+  uint32_t km, kc, vc, vs, vz;
 };
 
 template <int BK, int BV>
-__device__ __forceinline__ void load_block(const DecodeArgs& a, const uint8_t* blk, int j, int sub, int lane,
-                                           int gsel, int ng, BlockData<BK, BV>& o) {
-  const int col = lane & 15, row = lane >> 4;
-  const uint8_t* kmeta = blk + a.km + (size_t)j * 2 * kHeadDim * 2;
-  o.s = reinterpret_cast<const uint32_t*>(kmeta)[lane];
-  o.z = reinterpret_cast<const uint32_t*>(kmeta + kHeadDim * 2)[lane];
-  const int tok = j * a.gk + sub * 32;
+__device__ __forceinline__ void load_block(__amdgpu_buffer_rsrc_t r, const LaneOffsets& lo, uint32_t km,
+                                           uint32_t kc, uint32_t vc, uint32_t vm, BlockData<BK, BV>& o) {
+  o.s = ld32(r, lo.km, km);
+  o.z = ld32(r, lo.km + kHeadDim * 2, km);
 #pragma unroll
   for (int mb = 0; mb < 2; ++mb) {
-    const uint32_t* kr =
-        reinterpret_cast<const uint32_t*>(blk + a.kc + (size_t)(tok + 16 * mb + col) * 16 * BK) + BK * row;
     if constexpr (BK == 1) {
-      o.kx[mb][0] = kr[0];
+      o.kx[mb][0] = ld32(r, lo.kc + mb * 16 * 16 * BK, kc);
     } else {
-      const uint2 v = *reinterpret_cast<const uint2*>(kr);
+      const uint2 v = ld64(r, lo.kc + mb * 16 * 16 * BK, kc);
       o.kx[mb][0] = v.x;
       o.kx[mb][1] = v.y;
     }
   }
-  const int vb = tok / 32;
-  const uint32_t* vr = reinterpret_cast<const uint32_t*>(blk + a.vc + (size_t)vb * 512 * BV) + lane * 2 * BV;
   if constexpr (BV == 1) {
-    const uint2 v = *reinterpret_cast<const uint2*>(vr);
+    const uint2 v = ld64(r, lo.vc, vc);
     o.vx[0] = v.x;
     o.vx[1] = v.y;
   } else {
-    const uint4 v = *reinterpret_cast<const uint4*>(vr);
-    o.vx[0] = v.x; o.vx[1] = v.y; o.vx[2] = v.z; o.vx[3] = v.w;
+    const u4_t v = ld128(r, lo.vc, vc);
+    o.vx[0] = v[0]; o.vx[1] = v[1]; o.vx[2] = v[2]; o.vx[3] = v[3];
   }
-  const uint8_t* vmb = blk + a.vm + (size_t)vb * 128 * ng;
-  o.s01 = *reinterpret_cast<const uint2*>(vmb + value_meta_s(gsel, 4 * row));
-  o.s23 = *reinterpret_cast<const uint2*>(vmb + value_meta_s(gsel, 16 + 4 * row));
-  o.z01 = *reinterpret_cast<const uint2*>(vmb + value_meta_z(gsel, 4 * row, ng));
-  o.z23 = *reinterpret_cast<const uint2*>(vmb + value_meta_z(gsel, 16 + 4 * row, ng));
+  o.sv = ld128(r, lo.vs, vm);
+  o.zv = ld128(r, lo.vz, vm);
 }
 
-template <int BK, int BV>
+// The value of quad member K, broadcast to the whole quad (quad_perm
+// [K,K,K,K]; every lane has a source, so no fill value is needed).
+template <int K>
+__device__ __forceinline__ float quad_bcast(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), K * 0x55, 0xF, 0xF, false));
+}
+
+template <int BK, int BV, int BPG>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void decode_mfma_kernel(DecodeArgs a) {
   __shared__ uint32_t q_lds[kWaves][(2 * kGQ + 1) * kQRow];  // Q' hi rows, lo rows, key zero-points
   __shared__ float qp_lds[kWaves][kHeadDim * kGQ];  // fp16 tail split only
@@ -162,6 +185,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
   const int hc = col >> 2, xc = col & 3, part = col & 1;
   const int ng = kHeadDim / a.gv, gsel = xc & (ng - 1);
   const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * kGQ) * kHeadDim;
+  const __amdgpu_buffer_rsrc_t rs = head_rsrc(blk, a.head_stride);
+  LaneOffsets lo;
+  lo.km = 4 * lane;
+  lo.kc = col * 16 * BK + row * 4 * BK;
+  lo.vc = lane * 8 * BV;
+  lo.vs = (gsel * 32 + 8 * row) * 2;
+  lo.vz = lo.vs + ng * 64;
 
   // q~ = q * 2^-e per head with max |q~| < 1.  For the code MFMA each lane's
   // channel pair (2*lane, 2*lane+1) also carries 2^-w, w = the bit weight of
@@ -197,6 +227,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
     }
   }
 
+  // m, l: running maximum and denominator (l holds this lane's own token
+  // pairs only); zacc: the value zero-point term of the lane's group
   float m = -__builtin_inff(), l = 0.f, zacc = 0.f;
   f4_t acc[8];
 #pragma unroll
@@ -207,16 +239,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
   uint32_t* ql = q_lds[wv];
 
   // This wave's 32-token blocks: key groups j0 + wv + kWaves*n, each of
-  // gk/32 blocks.  Loads run one block ahead of the arithmetic.
-  const int bpg = a.gk / 32;
+  // BPG blocks.
   const int j0 = t0 / a.gk + wv, jend = t1 / a.gk;
   const int ngroups = j0 < jend ? (jend - j0 + kWaves - 1) / kWaves : 0;
-  const int nblocks = ngroups * bpg;
+  const int nblocks = ngroups * BPG;
+
+  // lanes whose quad member index has bit 0 / bit 1 set
+  const bool xb0 = xc & 1, xb1 = xc & 2;
 
   f4_t dz = {0.f, 0.f, 0.f, 0.f};
   h8_t bp[4];
   auto process = [&](const BlockData<BK, BV>& cur, int i) {
-    if (i % bpg == 0) {
+    if (BPG == 1 || i % BPG == 0) {
       // Q' = q~ (.) s of the block's key group, hi and lo halves, and the
       // group's zero-points, re-laid out through LDS
       wave_lds_sync();
@@ -242,7 +276,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
       dz *= 0x1p-24f;  // to the scale of the code products
     }
 
-    // scores of tokens 16*mb + 4*row + e of the block, e < 4
+    // unscaled scores (hi + lo) of tokens t = 4*mb + e, token 16*mb + 4*row + e
     f4_t d[2];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
@@ -252,52 +286,54 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
 #pragma unroll
         for (int p = 0; p < BK; ++p) d[mb] = mfma(unpack8(cur.kx[mb][p], kb, p), bp[kb], d[mb]);
     }
-    float sc[8];
+    float raw[8];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float v = d[mb][e];
-        sc[4 * mb + e] = (v + dpp_mov<kQuadXor1>(0.f, v)) * cs;
-      }
+      for (int e = 0; e < 4; ++e) raw[4 * mb + e] = d[mb][e] + dpp_mov<kQuadXor1>(0.f, d[mb][e]);
 
-    // online softmax (base 2) for head hc over these 32 tokens
-    float bm = sc[0];
-#pragma unroll
-    for (int t = 1; t < 8; ++t) bm = fmaxf(bm, sc[t]);
-    bm = max_across_rows(bm);
+    // online softmax (base 2) for head hc over these 32 tokens; cs > 0, so
+    // the maximum is taken before scaling
+    float bm = fmaxf(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])),
+                     fmaxf(fmaxf(raw[4], raw[5]), fmaxf(raw[6], raw[7])));
+    bm = max_across_rows(bm) * cs;
     const float mnew = fmaxf(m, bm);
     const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     m = mnew;
-    float p[8], ps = 0.f;
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      p[t] = __builtin_amdgcn_exp2f(sc[t] - mnew);
-      ps += p[t];
-    }
-    l = fmaf(l, alpha, ps);
+    // the four lanes of a quad hold the same eight scores: member k takes
+    // the exponentials of token pair k, then every member gets all eight
+    const float r0 = xb1 ? (xb0 ? raw[6] : raw[4]) : (xb0 ? raw[2] : raw[0]);
+    const float r1 = xb1 ? (xb0 ? raw[7] : raw[5]) : (xb0 ? raw[3] : raw[1]);
+    const float e0 = __builtin_amdgcn_exp2f(fmaf(r0, cs, -mnew));
+    const float e1 = __builtin_amdgcn_exp2f(fmaf(r1, cs, -mnew));
+    l = fmaf(l, alpha, e0 + e1);
+    float p[8];
+    p[0] = quad_bcast<0>(e0); p[1] = quad_bcast<0>(e1);
+    p[2] = quad_bcast<1>(e0); p[3] = quad_bcast<1>(e1);
+    p[4] = quad_bcast<2>(e0); p[5] = quad_bcast<2>(e1);
+    p[6] = quad_bcast<3>(e0); p[7] = quad_bcast<3>(e1);
     if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) acc[mb] *= alpha;
       zacc *= alpha;
     }
 
-    // P' = p * s_v in hi / lo halves; element pair t = tokens of p[2t], p[2t+1]
-    const uint32_t sv[4] = {cur.s01.x, cur.s01.y, cur.s23.x, cur.s23.y};
-    const uint32_t zv[4] = {cur.z01.x, cur.z01.y, cur.z23.x, cur.z23.y};
+    // P' = p * s_v as fp16 hi + lo: the product and its residual are each
+    // one mixed-precision fma from the fp32 p and the fp16 scale; element
+    // pair t also carries 2^-t, the inverse of its bit weight in the
+    // unpacked value operand
     u4_t bhi, blo;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const h2_t ph = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(p[2 * t], p[2 * t + 1]));
-      const h2_t pl = __builtin_bit_cast(
-          h2_t, __builtin_amdgcn_cvt_pkrtz(p[2 * t] - (float)ph.x, p[2 * t + 1] - (float)ph.y));
-      // value scale times 2^-t, the inverse of the pair's bit weight
-      const h2_t s2 = t == 0 ? u2h(sv[t]) : u2h(sv[t]) * (h2_t){(_Float16)(1.f / (1 << t)), (_Float16)(1.f / (1 << t))};
-      const h2_t hi = ph * s2;
-      const h2_t lo = __builtin_elementwise_fma(pl, s2, __builtin_elementwise_fma(ph, s2, -hi));
+      const h2_t s2 = t == 0 ? u2h(cur.sv[t])
+                             : u2h(cur.sv[t]) * (h2_t){(_Float16)(1.f / (1 << t)), (_Float16)(1.f / (1 << t))};
+      const float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
+      const h2_t hi = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(f0, f1));
+      const float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
+      const float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
       bhi[t] = h2u(hi);
-      blo[t] = h2u(lo);
-      const h2_t z2 = u2h(zv[t]);
+      blo[t] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(g0, g1));
+      const h2_t z2 = u2h(cur.zv[t]);
       zacc = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc));
     }
     const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
@@ -311,33 +347,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
       }
     }
   };
-  // block i of this wave: key group j0 + kWaves*(i / bpg), 32-token part i % bpg
+  // block i of this wave: key group j0 + kWaves*(i / BPG), 32-token part i % BPG
+  const int vstride = 128 * ng;
   auto load = [&](int i, BlockData<BK, BV>& o) {
-    load_block<BK, BV>(a, blk, j0 + kWaves * (i / bpg), i % bpg, lane, gsel, ng, o);
+    const int j = j0 + kWaves * (i / BPG);
+    const int tok = j * a.gk + (i % BPG) * 32;
+    load_block<BK, BV>(rs, lo, a.km + (uint32_t)j * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
+                       a.vc + (uint32_t)(tok / 32) * 512 * BV, a.vm + (uint32_t)(tok / 32) * vstride, o);
   };
 
   // Three buffers, loads two blocks ahead of the arithmetic.  The loads are
   // unconditional (past the end they re-read the last block) so every path
   // through the loop has the same loads in flight and the memory waits stay
-  // exact.
+  // exact; the main loop has no early exit, the last one or two blocks run
+  // after it.
   if (nblocks > 0) {
     const int last = nblocks - 1;
     BlockData<BK, BV> b0, b1, b2;
     load(0, b0);
     load(min(1, last), b1);
-    for (int i = 0; i < nblocks; i += 3) {
+    int i = 0;
+    for (; i + 3 <= nblocks; i += 3) {
       load(min(i + 2, last), b2);
       process(b0, i);
-      if (i + 1 >= nblocks) break;
       load(min(i + 3, last), b0);
       process(b1, i + 1);
-      if (i + 2 >= nblocks) break;
       load(min(i + 4, last), b1);
       process(b2, i + 2);
     }
+    if (i < nblocks) process(b0, i);
+    if (i + 1 < nblocks) process(b1, i + 1);
   }
 
-  // sums over the lane rows; the lanes of one head agree on m and l
+  // sums over the quad (l holds own token pairs) and over the lane rows;
+  // the lanes of one head then agree on m and l
+  l += dpp_mov<kQuadXor1>(0.f, l);
+  l += dpp_mov<kQuadXor2>(0.f, l);
   l += __shfl_xor(l, 16);
   l += __shfl_xor(l, 32);
   zacc += __shfl_xor(zacc, 16);
@@ -358,24 +403,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void d
   write_record<kGQ>(a, S, wk.h, wk.sp, red);
 }
 
-template <int BK, int BV>
+template <int BK, int BV, int BPG>
 int launch_t(const DecodeArgs& a, void* stream) {
-  hipLaunchKernelGGL((decode_mfma_kernel<BK, BV>), dim3(a.total_wg), dim3(64 * kWaves), 0, (hipStream_t)stream, a);
+  hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG>), dim3(a.total_wg), dim3(64 * kWaves), 0, (hipStream_t)stream,
+                     a);
   return (int)hipGetLastError();
+}
+
+template <int BK, int BV>
+int launch_bpg(const DecodeArgs& a, void* stream) {
+  switch (a.gk / 32) {
+    case 1: return launch_t<BK, BV, 1>(a, stream);
+    case 2: return launch_t<BK, BV, 2>(a, stream);
+    case 4: return launch_t<BK, BV, 4>(a, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
 
-bool matrix_decode_supported(int bk, int bv, int gq, int gv) {
-  return gq == kGQ && (bk == 1 || bk == 2) && (bv == 1 || bv == 2) && gv >= 32;
+bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes) {
+  return gq == kGQ && (bk == 1 || bk == 2) && (bv == 1 || bv == 2) && gv >= 32 && head_bytes <= 0xFFFFFFFFull;
 }
 
 int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, void* stream) {
   if (a.total_wg <= 0) return 0;
-  if (bk == 1 && bv == 1) return launch_t<1, 1>(a, stream);
-  if (bk == 1 && bv == 2) return launch_t<1, 2>(a, stream);
-  if (bk == 2 && bv == 1) return launch_t<2, 1>(a, stream);
-  if (bk == 2 && bv == 2) return launch_t<2, 2>(a, stream);
+  if (bk == 1 && bv == 1) return launch_bpg<1, 1>(a, stream);
+  if (bk == 1 && bv == 2) return launch_bpg<1, 2>(a, stream);
+  if (bk == 2 && bv == 1) return launch_bpg<2, 1>(a, stream);
+  if (bk == 2 && bv == 2) return launch_bpg<2, 2>(a, stream);
   return (int)hipErrorInvalidValue;
 }
 

@@ -206,7 +206,7 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   c->Lq.assign(d->batch, 0);
   for (int i = 0; i < d->batch; ++i)
     c->matrix.push_back(kvq::matrix_decode_supported(c->bk[i], c->bv[i], d->num_q_heads / d->num_kv_heads,
-                                                     d->value_group) ? 1 : 0);
+                                                     d->value_group, c->lay[i].stride) ? 1 : 0);
   *out = c;
   return ok();
 }

@@ -135,7 +135,10 @@ struct ExportArgs {
 int launch_append(const AppendArgs& a, int bk, int bv, void* stream);
 int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
 int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, void* stream);
-bool matrix_decode_supported(int bk, int bv, int gq, int gv);
+// Matrix-core decode (and the matrix layout) for this bit class: 4 query
+// heads per kv head, 1- or 2-bit codes, value groups >= 32 channels, and a
+// (sequence, head) block that one buffer resource covers.
+bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes);
 int launch_export(const ExportArgs& a, void* stream);
 int launch_merge(const MergeArgs& a, void* stream);
 int launch_dequant(const DequantArgs& a, void* stream);

@@ -13,16 +13,18 @@
 //      lives in dword b*g + p (bit plane p of its code) at bit
 //      pair_bit(kb, e) = 16*(e&1) + 8*(kb>>1) + 4*(kb&1) + (e>>1).
 //      Bits (pair_bit, pair_bit + 16) then hold a consecutive element pair,
-//      which one AND and one 24-bit multiply turn into two fp16 values.
+//      which one AND turns into two fp16 values (exact subnormal powers of 2).
 //    value codes: blocks of 32 tokens, 512*b bytes each, in the lane order of
 //      the MFMA A-operand of O^T = V^T P: lane L = c%16 + 16*kg holds 2*b
 //      dwords; dword d*b + p covers channel blocks mb = 4d + m4 (m4 in 0..3),
 //      channel c = 16*mb + c%16, and the K-index element e' (0..7) at bit
 //      pair_bit(m4, e'), for block token r = tau(8*kg + e') where
 //      tau(8*kg + e') = 4*kg + e' for e' < 4 and 16 + 4*kg + (e' - 4) otherwise.
-//    value meta: per 32-token block, scales s[g][r] then zeros z[g][r]
-//      (fp16, g < 128/Gv, r < 32): 128*(128/Gv) bytes, the same total as the
-//      canonical [t][g][(s, z)] order.
+//    value meta: per 32-token block, scales s[g][pos(r)] then zeros
+//      z[g][pos(r)] (fp16, g < 128/Gv, r < 32): 128*(128/Gv) bytes, the same
+//      total as the canonical [t][g][(s, z)] order.  pos = tau^-1 puts the 8
+//      tokens of K-group kg (lanes 16*kg .. 16*kg + 15) in 16 contiguous bytes,
+//      in B-fragment element order.
 //    key meta is [group][s[128], z[128]] in both layouts.
 #pragma once
 
@@ -60,8 +62,12 @@ KVQ_HD inline BitLoc value_bit(int r, int c, int p, int b) {
   return {lane * 2 * b + d * b + p, pair_bit(m4, e)};
 }
 
+// Position of block token r in a value meta row: tau^-1, so that
+// r = tau(pos) with tau(8*kg + e') = 4*kg + e' (e' < 4), 16 + 4*kg + e' - 4.
+KVQ_HD inline int value_meta_pos(int r) { return 8 * ((r & 15) >> 2) + 4 * (r >> 4) + (r & 3); }
+
 // Byte offsets of a value block's scale and zero of (group g, token r).
-KVQ_HD inline int value_meta_s(int g, int r) { return (g * 32 + r) * 2; }
-KVQ_HD inline int value_meta_z(int g, int r, int ng) { return (ng * 32 + g * 32 + r) * 2; }
+KVQ_HD inline int value_meta_s(int g, int r) { return (g * 32 + value_meta_pos(r)) * 2; }
+KVQ_HD inline int value_meta_z(int g, int r, int ng) { return (ng * 32 + g * 32 + value_meta_pos(r)) * 2; }
 
 }  // namespace kvq
