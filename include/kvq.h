@@ -112,7 +112,8 @@ size_t kvq_workspace_bytes(const kvq_cache* cache);
 /* Single-token decode attention over every cached token of every sequence:
  *   out[i][h][:] = softmax(q[i][h] . K^[i][kv(h)]^T / sqrt(d)) V^[i][kv(h)]
  * with kv(h) = h / (Hq / Hkv), K^ and V^ the dequantized cache (fp16 tail
- * tokens exact).  q: device fp16 [batch][Hq][d].  out: device fp32
+ * tokens exact).  q: device fp16 [batch][Hq][d], finite (a NaN or infinity
+ * in q gives undefined outputs for its rows).  out: device fp32
  * [batch][Hq][d].  ws: device scratch of ws_bytes >= kvq_workspace_bytes,
  * 16-byte aligned, contents undefined on entry and exit.  A sequence with
  * no tokens yields zeros.  Split-K over tokens (flash-decoding) followed

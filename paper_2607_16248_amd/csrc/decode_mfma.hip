@@ -156,8 +156,16 @@ __device__ __forceinline__ float quad_bcast(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), K * 0x55, 0xF, 0xF, false));
 }
 
+// Waves per SIMD the instantiation is compiled for: three where its
+// registers fit 168 without spilling, else two.
 template <int BK, int BV, int BPG>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void decode_mfma_kernel(DecodeArgs a) {
+struct MatrixOcc {
+  static constexpr int value = (BK + BV <= 3 && BK * BV * BPG <= 2) ? 3 : 2;
+};
+
+template <int BK, int BV, int BPG>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MatrixOcc<BK, BV, BPG>::value))) void
+decode_mfma_kernel(DecodeArgs a) {
   __shared__ uint32_t q_lds[kWaves][(2 * kGQ + 1) * kQRow];  // Q' hi rows, lo rows, key zero-points
   __shared__ float qp_lds[kWaves][kHeadDim * kGQ];  // fp16 tail split only
   __shared__ float p_lds[kWaves][32 * kGQ];         // fp16 tail split only
@@ -421,6 +429,14 @@ int launch_bpg(const DecodeArgs& a, void* stream) {
 }
 
 }  // namespace
+
+int matrix_decode_occupancy(int bk, int bv, int gk) {
+  const int bpg = gk / 32;
+  if (bk == 1 && bv == 1) return bpg == 1 ? MatrixOcc<1, 1, 1>::value : bpg == 2 ? MatrixOcc<1, 1, 2>::value : MatrixOcc<1, 1, 4>::value;
+  if (bk == 1 && bv == 2) return bpg == 1 ? MatrixOcc<1, 2, 1>::value : bpg == 2 ? MatrixOcc<1, 2, 2>::value : MatrixOcc<1, 2, 4>::value;
+  if (bk == 2 && bv == 1) return bpg == 1 ? MatrixOcc<2, 1, 1>::value : bpg == 2 ? MatrixOcc<2, 1, 2>::value : MatrixOcc<2, 1, 4>::value;
+  return bpg == 1 ? MatrixOcc<2, 2, 1>::value : bpg == 2 ? MatrixOcc<2, 2, 2>::value : MatrixOcc<2, 2, 4>::value;
+}
 
 bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes) {
   return gq == kGQ && (bk == 1 || bk == 2) && (bv == 1 || bv == 2) && gv >= 32 && head_bytes <= 0xFFFFFFFFull;

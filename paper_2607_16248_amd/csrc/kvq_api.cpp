@@ -32,6 +32,7 @@ struct kvq_cache {
   std::vector<HeadLayout> lay;
   std::vector<int32_t> L, Lq;
   std::vector<uint8_t> matrix;  // 1: matrix layout and the matrix-core decode kernel
+  int occupancy = 2;             // resident decode workgroups per compute unit
   int32_t split_tokens = 0;
 };
 
@@ -41,21 +42,21 @@ thread_local std::string g_err;
 
 constexpr int kMaxSplits = 512;          // packed splits per sequence and kv head
 constexpr int kMinGroupsPerSplit = 4;    // one key group per wave at least
-constexpr int kWorkgroupsPerCU = 2;      // resident decode workgroups per compute unit
-
-// Decode workgroups that fit the current device at once (one round of the grid).
-int64_t target_workgroups() {
+// Decode workgroups that fit the current device at once (one round of the
+// grid): compute units times the resident workgroups per unit (one 4-wave
+// workgroup per wave slot of a SIMD).
+int64_t target_workgroups(int per_cu) {
   static thread_local int cached_dev = -1;
-  static thread_local int64_t cached = 0;
+  static thread_local int64_t cus = 0;
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 512;
+  if (hipGetDevice(&dev) != hipSuccess) return 256 * per_cu;
   if (dev != cached_dev) {
-    int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
     cached_dev = dev;
-    cached = (int64_t)cus * kWorkgroupsPerCU;
+    cus = n;
   }
-  return cached;
+  return cus * per_cu;
 }
 
 kvq_status fail(kvq_status s, const char* fmt, ...) {
@@ -126,7 +127,7 @@ int32_t split_tokens_for(const kvq_cache* c) {
     total += (int64_t)c->Lq[i] * c->d.num_kv_heads;
     lq_max = std::max<int64_t>(lq_max, c->Lq[i]);
   }
-  const int64_t target = target_workgroups();
+  const int64_t target = target_workgroups(c->occupancy);
   int64_t st = (total + target - 1) / target;
   st = std::max<int64_t>(st, (lq_max + kMaxSplits - 1) / kMaxSplits);
   st = (st + gk - 1) / gk * gk;
@@ -207,6 +208,11 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   for (int i = 0; i < d->batch; ++i)
     c->matrix.push_back(kvq::matrix_decode_supported(c->bk[i], c->bv[i], d->num_q_heads / d->num_kv_heads,
                                                      d->value_group, c->lay[i].stride) ? 1 : 0);
+  // the split plan fills one round of the lowest-occupancy kernel in use
+  c->occupancy = 3;
+  for (int i = 0; i < d->batch; ++i)
+    c->occupancy = std::min(c->occupancy, c->matrix[i] ? kvq::matrix_decode_occupancy(c->bk[i], c->bv[i], d->key_group)
+                                                        : 2);
   *out = c;
   return ok();
 }

@@ -139,6 +139,9 @@ int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, void* stream);
 // heads per kv head, 1- or 2-bit codes, value groups >= 32 channels, and a
 // (sequence, head) block that one buffer resource covers.
 bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes);
+// Waves per SIMD of the matrix-core kernel for this bit class (2 or 3); the
+// vector kernel runs two.
+int matrix_decode_occupancy(int bk, int bv, int gk);
 int launch_export(const ExportArgs& a, void* stream);
 int launch_merge(const MergeArgs& a, void* stream);
 int launch_dequant(const DequantArgs& a, void* stream);

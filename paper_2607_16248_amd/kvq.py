@@ -229,7 +229,10 @@ class KVCache:
     def __del__(self):
         h = getattr(self, "handle", None)
         if h:
-            kvq_cache_destroy(h)
+            try:
+                kvq_cache_destroy(h)
+            except TypeError:  # interpreter shutdown: module globals are already torn down
+                pass
             self.handle = None
 
     def append(self, K, V, n_new=None, stream=None):
