@@ -46,8 +46,9 @@ def matrix_path(w) -> bool:
 
 def source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("decode.hip", "decode_mfma.hip", "decode_common.h", "kvq_internal.h", "kvq_layout.h"):
-        with open(os.path.join(ROOT, "paper_2607_16248_amd", "csrc", f), "rb") as fh:
+    for f in ("csrc/decode.hip", "csrc/decode_mfma.hip", "csrc/decode_common.h", "csrc/kvq_internal.h",
+              "csrc/kvq_layout.h", "build.py"):
+        with open(os.path.join(ROOT, "paper_2607_16248_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
@@ -140,7 +141,8 @@ def main():
     appending = args.workload == 2
     layers = w.layers if w.layers > 1 else max(1, min(64, -(-(1 << 30) // max(1, sum(
         packed_bytes(L, w, bk, bv) for L, bk, bv in zip(w.lens, w.bits_k, w.bits_v))))))
-    extra = (steps + warm + 2) if appending else 0
+    append_rounds = 4  # extra appends per layer timed on their own after the steps
+    extra = (steps + warm + 2 + append_rounds) if appending else 0
     cap = max(w.lens) + extra
 
     log(f"[bench] workload {w.name}: {layers} layer caches, capacity {cap}")
@@ -170,7 +172,7 @@ def main():
     # appended tokens for every step, generated up front and resident on the device
     app = []
     if appending:
-        for st in range(steps + warm + 1):
+        for st in range(steps + warm + 1 + append_rounds):
             row = []
             for l in range(layers):
                 Kn, Vn = gen_append(w, l, 0, st)
@@ -235,6 +237,67 @@ def main():
     merge_us = timed(lambda i: kvq.kvq_decode_merge(handles[i % layers], ws, outs[i % layers], stream=stream), it)
     decode_us = timed(lambda i: kvq.kvq_decode_attention(handles[i % layers], qs[i % layers], outs[i % layers],
                                                          ws, ws_bytes, stream=stream), it)
+    # per-launch spread of the split kernel: one event pair per launch
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(64)]
+    for i, (a, b) in enumerate(pairs):
+        a.record()
+        kvq.kvq_decode_partials(handles[i % layers], qs[i % layers], ws, ws_bytes, stream=stream)
+        b.record()
+    torch.cuda.synchronize()
+    per_launch = sorted(a.elapsed_time(b) * 1e3 for a, b in pairs)
+    split_med = per_launch[len(per_launch) // 2]
+    split_p95 = per_launch[int(0.95 * (len(per_launch) - 1))]
+
+    # decode of every layer replayed from one captured graph (lengths are fixed
+    # between appends, so the launches of a decode are the same every replay);
+    # every replay must reproduce the eager outputs bit for bit
+    graph_us = None
+    graph_exact = None
+    try:
+        for l in range(layers):
+            kvq.kvq_decode_attention(handles[l], qs[l], outs[l], ws, ws_bytes, stream=stream)
+        torch.cuda.synchronize()
+        eager = [o.clone() for o in outs]
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            gs = torch.cuda.current_stream().cuda_stream
+            for l in range(layers):
+                kvq.kvq_decode_attention(handles[l], qs[l], outs[l], ws, ws_bytes, stream=gs)
+        graph_exact = True
+        for _ in range(3):
+            for o in outs:
+                o.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            graph_exact &= all(torch.equal(o, e) for o, e in zip(outs, eager))
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = max(4, it // layers)
+        a.record()
+        for _ in range(reps):
+            g.replay()
+        b.record()
+        torch.cuda.synchronize()
+        graph_us = a.elapsed_time(b) * 1e3 / (reps * layers)
+        del g
+    except RuntimeError as e:  # capture unsupported: report and go on
+        log(f"[bench] graph replay skipped: {e}")
+
+    # appends on their own: append_rounds more tokens per layer (copies into
+    # the fp16 ring; a key group flushes once every key_group tokens)
+    append_us = None
+    if appending:
+        base = warm + steps
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for r in range(append_rounds):
+            for l in range(layers):
+                kvq.kvq_append(handles[l], app[base + r][l][0], app[base + r][l][1], one, n_max=1, stream=stream)
+        b.record()
+        torch.cuda.synchronize()
+        append_us = a.elapsed_time(b) * 1e3 / (append_rounds * layers)
+        for c in caches:
+            c.check()
+
     L_now = [kvq.kvq_seq_len(handles[0], s) for s in range(w.batch)]
     launch_bytes = sum(packed_bytes(L, w, bk, bv) for L, bk, bv in zip(L_now, w.bits_k, w.bits_v))
     achieved = launch_bytes / (split_us * 1e-6) / 1e9
@@ -276,7 +339,12 @@ def main():
         "us_per_layer": round(us_per_layer, 3),
         "decode_us_per_layer": round(decode_us, 3),
         "split_kernel_us": round(split_us, 3),
+        "split_kernel_us_median": round(split_med, 3),
+        "split_kernel_us_p95": round(split_p95, 3),
         "merge_kernel_us": round(merge_us, 3),
+        "decode_graph_us_per_layer": None if graph_us is None else round(graph_us, 3),
+        "decode_graph_exact": graph_exact,
+        "append_us": None if append_us is None else round(append_us, 3),
         "bytes_per_layer": launch_bytes,
         "wall_s_timed": round(wall, 4),
         "roofline": {
@@ -286,7 +354,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]}>" if matrix_path(w) else
+            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.key_group // 32}>" if matrix_path(w) else
                        f"decode_split_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.group_q}>"),
             "bytes_per_launch": launch_bytes,
             "kernel_source_sha256_16": source_digest(),

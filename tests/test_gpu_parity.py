@@ -45,6 +45,8 @@ SMALL = [
     W("gq8_k8v8_gv16", 1, 64, 8, 600, 8, 8, gv=16),
     W("ragged_mixed", 4, 32, 8, (900, 64, 31, 1500), (2, 2, 4, 4), (2, 2, 4, 4), gk=64),
     W("window_bigger_than_L", 1, 32, 8, 100, 1, 1, R=300),
+    W("k1v1_g128_L1100", 1, 32, 8, 1100, 1, 1, gk=128),
+    W("mixed_asym_g64_gv64", 4, 32, 8, (700, 1300, 520, 64), (1, 2, 1, 2), (2, 1, 1, 2), gk=64, gv=64),
 ]
 
 
