@@ -184,11 +184,15 @@ def main():
     one = [1] * w.batch
     handles = [c.handle for c in caches]
 
+    # one decode step: every layer appends its token and attends (one call;
+    # the token is stored by the decode launch unless a key group fills)
     def step(st):
         for l in range(layers):
             if appending:
-                kvq.kvq_append(handles[l], app[st][l][0], app[st][l][1], one, n_max=1, stream=stream)
-            kvq.kvq_decode_attention(handles[l], qs[l], outs[l], ws, ws_bytes, stream=stream)
+                kvq.kvq_append_decode(handles[l], app[st][l][0], app[st][l][1], one, qs[l], outs[l], ws,
+                                      ws_bytes=ws_bytes, n_max=1, stream=stream)
+            else:
+                kvq.kvq_decode_attention(handles[l], qs[l], outs[l], ws, ws_bytes, stream=stream)
 
     log(f"[bench] warmup {warm} steps")
     for st in range(warm):

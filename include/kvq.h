@@ -122,6 +122,22 @@ size_t kvq_workspace_bytes(const kvq_cache* cache);
 kvq_status kvq_decode_attention(const kvq_cache* cache, const void* q, float* out, void* ws,
                                 size_t ws_bytes, void* stream);
 
+/* One decode step in one call: the same result, cache state and error
+ * behaviour as kvq_append(cache, K, V, n_max, n_new, stream) followed by
+ * kvq_decode_attention(cache, q, out, ws, ws_bytes, stream) (the decode is
+ * that of the Introduction's attention; the append is the quantize-on-append
+ * of kvq_append).  When the new tokens complete no key group (every step
+ * but one in key_group for single-token decode), the tokens stay fp16 and
+ * the decode launch itself stores them into the fp16 tail before it attends
+ * over them: two launches instead of three.  Otherwise it runs the two
+ * calls.  K, V: as for kvq_append, 4-byte aligned.  ws_bytes must cover the
+ * lengths after the append (kvq_workspace_bytes covers any length).  Every
+ * argument, capacity and workspace check happens before anything is
+ * launched, and a failed check leaves the cache unchanged. */
+kvq_status kvq_append_decode(kvq_cache* cache, const void* K, const void* V, int32_t n_max,
+                             const int32_t* n_new, const void* q, float* out, void* ws, size_t ws_bytes,
+                             void* stream);
+
 /* The two phases of kvq_decode_attention, for callers that combine partial
  * results themselves (for example across devices) and for timing.
  * kvq_decode_partials writes, for every sequence i, query head h and split

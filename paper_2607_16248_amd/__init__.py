@@ -3,7 +3,7 @@
 The computation lives in the HIP library libkvq.so (C ABI: include/kvq.h);
 :mod:`paper_2607_16248_amd.kvq` is its thin ctypes binding.
 """
-from .kvq import (KVCache, KvqError, kvq_append, kvq_cache_bytes, kvq_cache_destroy,  # noqa: F401
+from .kvq import (KVCache, KvqError, kvq_append, kvq_append_decode, kvq_cache_bytes, kvq_cache_destroy,  # noqa: F401
                   kvq_cache_init, kvq_cache_reset, kvq_check, kvq_decode_attention,
                   kvq_decode_merge, kvq_decode_partials, kvq_dequant,
                   kvq_export, kvq_export_bytes, kvq_last_error, kvq_seq_len, kvq_set_split_tokens,

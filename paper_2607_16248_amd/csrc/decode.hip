@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
     for (int j = t0 / a.gk + wv; j < t1 / a.gk; j += kWaves)
       packed_group<BK, BV, GQ>(a, blk, j, qs0, qs1, qp, pl, st, lane);
   } else {
-    tail_split<GQ>(a, S, blk, qs0, qs1, qp, pl, st, lane, wv);
+    tail_split<GQ>(a, S, wk.h, blk, qs0, qs1, qp, pl, st, lane, wv);
   }
   stage_state<GQ>(st, red, lane, wv);
   __syncthreads();

@@ -214,10 +214,28 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSe
 
 // The fp16 tail split: every wave takes passes of 32 tokens.
 template <int GQ>
-__device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq& S, const uint8_t* blk,
+__device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq& S, int h, const uint8_t* blk,
                                            const float (&qs0)[GQ], const float (&qs1)[GQ], float* qp,
                                            float* pl, State<GQ>& st, int lane, int wv) {
   constexpr int QS = QStride<GQ>::value;
+  // Fused append: this workgroup alone reads the ring of (sequence, head h)
+  // in this launch; it first stores the tokens appended by the call, which
+  // all stay fp16 (the host takes this path only when no key group fills).
+  if (a.K_new != nullptr && S.L_old < S.L) {
+    uint32_t* rk = reinterpret_cast<uint32_t*>(const_cast<uint8_t*>(blk) + a.tk);
+    uint32_t* rv = reinterpret_cast<uint32_t*>(const_cast<uint8_t*>(blk) + a.tv);
+    const uint32_t* ik = reinterpret_cast<const uint32_t*>(a.K_new);
+    const uint32_t* iv = reinterpret_cast<const uint32_t*>(a.V_new);
+    constexpr int kRow = kHeadDim / 2;  // dwords per token row
+    for (int idx = threadIdx.x; idx < (S.L - S.L_old) * kRow; idx += blockDim.x) {
+      const int t = idx / kRow, c = idx % kRow;
+      const size_t src = (((size_t)S.seq * a.n_max + t) * a.hkv + h) * kRow + c;
+      const size_t dst = (size_t)((S.L_old + t) % a.W) * kRow + c;
+      rk[dst] = ik[src];
+      rv[dst] = iv[src];
+    }
+    __syncthreads();  // the stores are visible to the whole workgroup
+  }
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
     qp[(2 * lane) * QS + g] = qs0[g];

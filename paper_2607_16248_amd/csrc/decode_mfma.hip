@@ -182,7 +182,7 @@ decode_mfma_kernel(DecodeArgs a) {
     load_q_scaled<kGQ>(a, S, wk.h, lane, qs0, qs1);
     State<kGQ> st;
     init_state<kGQ>(st);
-    tail_split<kGQ>(a, S, blk, qs0, qs1, qp_lds[wv], p_lds[wv], st, lane, wv);
+    tail_split<kGQ>(a, S, wk.h, blk, qs0, qs1, qp_lds[wv], p_lds[wv], st, lane, wv);
     stage_state<kGQ>(st, red, lane, wv);
     __syncthreads();
     write_record<kGQ>(a, S, wk.h, wk.sp, red);

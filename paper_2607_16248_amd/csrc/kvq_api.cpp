@@ -331,8 +331,18 @@ SplitPlan plan_splits(const kvq_cache* c) {
   return p;
 }
 
+// Append inputs of a fused append + decode: the tokens [L_old[i], L[i]) of
+// each sequence come from K/V rows and are written into the ring by the
+// decode launch itself.
+struct FusedAppend {
+  const void* K;
+  const void* V;
+  int32_t n_max;
+  const std::vector<int32_t>* L_old;
+};
+
 kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, void* ws, size_t ws_bytes,
-                        void* stream) {
+                        void* stream, const FusedAppend* app = nullptr) {
   const kvq_cache_desc& d = c->d;
   const size_t need = (size_t)p.records * d.num_q_heads * kvq::kRecFloats * sizeof(float);
   if (!q) return fail(KVQ_ERR_ARG, "q must be a device pointer");
@@ -355,11 +365,17 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.hq = d.num_q_heads; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
     a.split_tokens = p.split_tokens;
     a.qscale = qscale;
+    if (app) {
+      a.K_new = static_cast<const uint16_t*>(app->K);
+      a.V_new = static_cast<const uint16_t*>(app->V);
+      a.n_max = app->n_max;
+    }
     int wg = 0, n = 0;
     for (int i : cls.second) {
       kvq::DecodeSeq& s = a.seq[n++];
       s.head0 = c->head0[i];
       s.seq = i; s.L = c->L[i]; s.Lq = c->Lq[i];
+      s.L_old = app ? (*app->L_old)[i] : c->L[i];
       s.nq = p.nq[i]; s.nsplit = p.ns[i]; s.ws_base = p.base[i];
       s.wg_begin = wg;
       wg += p.ns[i] * d.num_kv_heads;
@@ -403,6 +419,59 @@ kvq_status kvq_decode_attention(const kvq_cache* c, const void* q, float* out, v
   if (!q || !out) return fail(KVQ_ERR_ARG, "q and out must be device pointers");
   const SplitPlan p = plan_splits(c);
   kvq_status st = run_partials(c, p, q, ws, ws_bytes, stream);
+  if (st != KVQ_OK) return st;
+  st = run_merge(c, p, ws, out, stream);
+  if (st != KVQ_OK) return st;
+  return ok();
+}
+
+kvq_status kvq_append_decode(kvq_cache* c, const void* K, const void* V, int32_t n_max, const int32_t* n_new,
+                             const void* q, float* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (!n_new) return fail(KVQ_ERR_ARG, "n_new is NULL");
+  if (n_max < 0) return fail(KVQ_ERR_ARG, "n_max must be >= 0");
+  if (!q || !out) return fail(KVQ_ERR_ARG, "q and out must be device pointers");
+  const kvq_cache_desc& d = c->d;
+  bool any = false, flush = false;
+  for (int i = 0; i < d.batch; ++i) {
+    if (n_new[i] < 0 || n_new[i] > n_max)
+      return fail(KVQ_ERR_ARG, "sequence %d: n_new = %d outside [0, n_max = %d]", i, n_new[i], n_max);
+    if ((int64_t)c->L[i] + n_new[i] > d.max_tokens)
+      return fail(KVQ_ERR_CAPACITY, "sequence %d: %d + %d tokens exceed max_tokens = %d", i, c->L[i], n_new[i],
+                  d.max_tokens);
+    any |= n_new[i] > 0;
+    flush |= quantized_len(c->L[i] + n_new[i], d) != c->Lq[i];
+  }
+  if (any && (!K || !V)) return fail(KVQ_ERR_ARG, "K and V must be device pointers");
+  if (any && (reinterpret_cast<uintptr_t>(K) % 4 != 0 || reinterpret_cast<uintptr_t>(V) % 4 != 0))
+    return fail(KVQ_ERR_ARG, "K and V must be 4-byte aligned");
+
+  // plan with the lengths after the append; nothing is launched or changed
+  // unless the workspace fits
+  const std::vector<int32_t> L_old = c->L, Lq_old = c->Lq;
+  for (int i = 0; i < d.batch; ++i) {
+    c->L[i] = L_old[i] + n_new[i];
+    c->Lq[i] = quantized_len(c->L[i], d);
+  }
+  const SplitPlan p = plan_splits(c);
+  const size_t need = (size_t)p.records * d.num_q_heads * kvq::kRecFloats * sizeof(float);
+  const char* bad = nullptr;
+  kvq_status bad_st = KVQ_ERR_ARG;
+  if (need > 0 && !ws) bad = "workspace is NULL";
+  else if (ws_bytes < need) bad = "workspace too small for the lengths after the append", bad_st = KVQ_ERR_CAPACITY;
+  else if (reinterpret_cast<uintptr_t>(ws) % 16 != 0) bad = "workspace must be 16-byte aligned";
+  if (bad || flush) {
+    c->L = L_old;
+    c->Lq = Lq_old;
+  }
+  if (bad) return fail(bad_st, "%s (needs %zu bytes, has %zu)", bad, need, ws_bytes);
+  if (flush) {  // a key group fills: the append kernel packs it, then a plain decode
+    kvq_status st = kvq_append(c, K, V, n_max, n_new, stream);
+    if (st != KVQ_OK) return st;
+    return kvq_decode_attention(c, q, out, ws, ws_bytes, stream);
+  }
+  const FusedAppend app{K, V, n_max, &L_old};
+  kvq_status st = run_partials(c, p, q, ws, ws_bytes, stream, any ? &app : nullptr);
   if (st != KVQ_OK) return st;
   st = run_merge(c, p, ws, out, stream);
   if (st != KVQ_OK) return st;

@@ -81,13 +81,19 @@ struct DecodeSeq {
   int32_t nsplit;     // nq + (L > Lq)
   int32_t wg_begin;
   int32_t ws_base;    // first split record of this sequence
-  int32_t pad;
+  int32_t L_old;      // tokens [L_old, L) arrive in this call (fused append), else L_old = L
 };
 
 struct DecodeArgs {
   const uint8_t* arena;
   const uint16_t* q;  // fp16 [batch][Hq][128]
   float* ws;          // split records [.][Hq][kRecFloats]
+  // fused append: fp16 [batch][n_max][Hkv][128] rows of the tokens [L_old, L),
+  // written into the ring by the fp16 tail split of their (sequence, head)
+  // before it attends over them; null when the call appends nothing
+  const uint16_t* K_new;
+  const uint16_t* V_new;
+  int32_t n_max, pad;
   uint64_t head_stride;
   uint32_t kc, km, vc, vm, tk, tv;
   int32_t hq, hkv, gk, gv, W, split_tokens, nseq, total_wg;

@@ -19,7 +19,7 @@ STATUS_NAMES = ["KVQ_OK", "KVQ_ERR_ARG", "KVQ_ERR_UNSUPPORTED", "KVQ_ERR_CAPACIT
                 "KVQ_ERR_RANGE", "KVQ_ERR_STATE", "KVQ_ERR_HIP"]
 
 EXPORTED = ["kvq_cache_bytes", "kvq_cache_init", "kvq_cache_destroy", "kvq_cache_reset",
-            "kvq_seq_len", "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention",
+            "kvq_seq_len", "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention", "kvq_append_decode",
             "kvq_decode_partials", "kvq_decode_merge",
             "kvq_dequant", "kvq_export_bytes", "kvq_export", "kvq_check",
             "kvq_set_split_tokens", "kvq_last_error", "kvq_version"]
@@ -63,6 +63,7 @@ def lib():
         "kvq_append": ([P, P, P, I32, ctypes.POINTER(I32), P], ctypes.c_int),
         "kvq_workspace_bytes": ([P], S),
         "kvq_decode_attention": ([P, P, P, P, S, P], ctypes.c_int),
+        "kvq_append_decode": ([P, P, P, I32, ctypes.POINTER(I32), P, P, P, S, P], ctypes.c_int),
         "kvq_decode_partials": ([P, P, P, S, P], ctypes.c_int),
         "kvq_decode_merge": ([P, P, P, P], ctypes.c_int),
         "kvq_dequant": ([P, I32, I32, I32, P, P, P], ctypes.c_int),
@@ -163,6 +164,18 @@ def kvq_decode_attention(cache: int, q, out, ws, ws_bytes: Optional[int] = None,
     _check(lib().kvq_decode_attention(cache, _ptr(q), _ptr(out), _ptr(ws), int(ws_bytes), _stream(stream)))
 
 
+def kvq_append_decode(cache: int, K, V, n_new: Sequence[int], q, out, ws, ws_bytes: Optional[int] = None,
+                      n_max: Optional[int] = None, stream=None) -> None:
+    """kvq_append then kvq_decode_attention in one call (two launches when no key group fills)."""
+    n = (ctypes.c_int32 * max(1, len(n_new)))(*n_new)
+    if n_max is None:
+        n_max = int(K.shape[1]) if K is not None and not isinstance(K, int) else max(n_new, default=0)
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().kvq_append_decode(cache, _ptr(K), _ptr(V), int(n_max), n, _ptr(q), _ptr(out), _ptr(ws),
+                                   int(ws_bytes), _stream(stream)))
+
+
 def kvq_decode_partials(cache: int, q, ws, ws_bytes: Optional[int] = None, stream=None) -> None:
     """Phase 1 of decode: per-split softmax records into ``ws``."""
     if ws_bytes is None:
@@ -253,6 +266,16 @@ class KVCache:
             out = torch.empty((self.batch, self.num_q_heads, self.head_dim), dtype=torch.float32,
                               device=q.device)
         kvq_decode_attention(self.handle, q, out, self.workspace(), stream=stream)
+        return out
+
+    def append_decode(self, K, V, q, n_new=None, out=None, stream=None):
+        import torch
+        if n_new is None:
+            n_new = [int(K.shape[1])] * self.batch
+        if out is None:
+            out = torch.empty((self.batch, self.num_q_heads, self.head_dim), dtype=torch.float32,
+                              device=q.device)
+        kvq_append_decode(self.handle, K, V, n_new, q, out, self.workspace(), stream=stream)
         return out
 
     def seq_len(self, seq):

@@ -131,6 +131,33 @@ def test_append_errors_leave_cache_unchanged():
         kvq.kvq_cache_destroy(h)
 
 
+def test_append_decode_errors_leave_cache_unchanged():
+    """Every check of the fused append + decode precedes any launch."""
+    d = desc(batch=2, bits_k=[1, 4], bits_v=[1, 4], max_tokens=100)
+    h = kvq.kvq_cache_init(d, FAKE_ARENA, kvq.kvq_cache_bytes(d))
+    F = FAKE_ARENA
+    try:
+        cases = [
+            (dict(K=F, V=F, n_new=[101, 0], n_max=200), kvq.ERR_CAPACITY),
+            (dict(K=F, V=F, n_new=[11, 0], n_max=10), kvq.ERR_ARG),
+            (dict(K=F, V=F, n_new=[1, 0], n_max=1, q=None), kvq.ERR_ARG),
+            (dict(K=None, V=F, n_new=[1, 0], n_max=1), kvq.ERR_ARG),
+            (dict(K=F + 2, V=F, n_new=[1, 0], n_max=1), kvq.ERR_ARG),
+            (dict(K=F, V=F, n_new=[5, 3], n_max=5, ws_bytes=16), kvq.ERR_CAPACITY),
+            (dict(K=F, V=F, n_new=[5, 3], n_max=5, ws=F + 8, ws_bytes=1 << 20), kvq.ERR_ARG),
+        ]
+        for kw, status in cases:
+            args = dict(q=F, out=F, ws=F, ws_bytes=1 << 20)
+            args.update(kw)
+            with pytest.raises(kvq.KvqError) as e:
+                kvq.kvq_append_decode(h, args["K"], args["V"], args["n_new"], args["q"], args["out"], args["ws"],
+                                      ws_bytes=args["ws_bytes"], n_max=args["n_max"])
+            assert e.value.status == status, kw
+            assert kvq.kvq_seq_len(h, 0) == 0 and kvq.kvq_seq_len(h, 1) == 0, kw
+    finally:
+        kvq.kvq_cache_destroy(h)
+
+
 def test_split_setting_and_workspace_bound():
     d = desc(max_tokens=131072, bits_k=[1], bits_v=[1])
     h = kvq.kvq_cache_init(d, FAKE_ARENA, kvq.kvq_cache_bytes(d))

@@ -203,3 +203,41 @@ def test_full_workload_3_sampled():
 def test_full_workload_4_sampled(bits):
     w = workload(4, bits)
     _sampled_parity(w, [(0, 3), (3, 6)])
+
+
+FUSED = [
+    W("fused_k1v1_matrix", 2, 32, 8, (300, 45), 1, 1),
+    W("fused_gq5_k2v2_R128", 2, 40, 8, (200, 31), 2, 2, R=128, dist="student_t3"),
+    W("fused_mixed_g64", 3, 32, 8, (130, 64, 0), (1, 2, 4), (1, 2, 4), gk=64),
+]
+
+
+@pytest.mark.parametrize("w", FUSED, ids=[w.name for w in FUSED])
+def test_append_decode_matches_separate_calls(w):
+    """kvq_append_decode gives the bytes, lengths and outputs of kvq_append
+    followed by kvq_decode_attention, bit for bit, across key-group flushes."""
+    import torch
+    steps = 40
+    a = Case(w, max_tokens=max(w.lens) + 2 * steps + 2)
+    b = Case(w, max_tokens=max(w.lens) + 2 * steps + 2)
+    a.append_all()
+    b.append_all()
+    rng = np.random.default_rng(7)
+    for st in range(steps):
+        n_new = [int(x) for x in rng.integers(0, 3, size=w.batch)]
+        if st % 5 == 0:
+            n_new = [1] * w.batch
+        nmax = max(max(n_new), 1)
+        Kn = torch.from_numpy(rng.standard_normal((w.batch, nmax, w.num_kv_heads, 128)).astype(np.float16)).cuda()
+        Vn = torch.from_numpy(rng.standard_normal((w.batch, nmax, w.num_kv_heads, 128)).astype(np.float16)).cuda()
+        out_a = a.cache.append_decode(Kn, Vn, a.qd, n_new=n_new)
+        b.cache.append(Kn, Vn, n_new)
+        out_b = b.cache.decode(b.qd)
+        torch.cuda.synchronize()
+        assert [a.cache.seq_len(s) for s in range(w.batch)] == [b.cache.seq_len(s) for s in range(w.batch)]
+        assert torch.equal(out_a, out_b), (w.name, st, n_new)
+    a.cache.check()
+    for s in range(w.batch):
+        for h in range(w.num_kv_heads):
+            assert np.array_equal(a.cache.export(s, h), b.cache.export(s, h)), (w.name, s, h)
+    log(f"[fused] {w.name}: {steps} steps bit-identical to separate append + decode")
