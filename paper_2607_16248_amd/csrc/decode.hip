@@ -151,31 +151,19 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   write_record<GQ>(a, S, wk.h, wk.sp, red);
 }
 
-// One workgroup per (sequence, query head): the split maxima and weights are
-// computed in parallel over splits, then each thread sums one channel over
-// half of the splits with independent loads.
-constexpr int kMergeThreads = 256;
-constexpr int kMaxMergeSplits = 1024;
-
-__device__ __forceinline__ float block_reduce(float v, bool is_max, float* scratch) {
-  v = is_max ? wave_max(v) : wave_sum(v);
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  if (lane == 0) scratch[wv] = v;
-  __syncthreads();
-  float r = scratch[0];
-#pragma unroll
-  for (int w = 1; w < kMergeThreads / 64; ++w) r = is_max ? fmaxf(r, scratch[w]) : r + scratch[w];
-  __syncthreads();
-  return r;
-}
+// One workgroup per (sequence, query head): thread (part, c) folds the
+// records of splits part, part + 8, ... into a running (max, denominator,
+// channel c numerator), loading kMergeUnroll records at a time so that one
+// memory round trip covers them; the eight parts then meet in LDS.
+constexpr int kMergeParts = 8;
+constexpr int kMergeThreads = kMergeParts * kHeadDim;
+constexpr int kMergeUnroll = 16;
 
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
-  __shared__ float wts[kMaxMergeSplits];
-  __shared__ float scratch[kMergeThreads / 64];
-  __shared__ float part[2][kHeadDim];
+  __shared__ float sm[kMergeParts], sl[kMergeParts], sa[kMergeParts][kHeadDim];
   const int si = blockIdx.x / a.hq, hq = blockIdx.x % a.hq;
   const MergeSeq& S = a.seq[si];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, c = tid % kHeadDim, part = tid / kHeadDim;
   float* o = a.out + ((size_t)S.seq * a.hq + hq) * kHeadDim;
   const int n = S.nsplit;
   if (n == 0) {
@@ -184,27 +172,53 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
   }
   const float* base = a.ws + ((size_t)S.ws_base * a.hq + hq) * kRecFloats;
   const size_t step = (size_t)a.hq * kRecFloats;
-  float mx = -__builtin_inff();
-  for (int i = tid; i < n; i += kMergeThreads) {
-    const float m = base[i * step];
-    wts[i] = m;
-    mx = fmaxf(mx, m);
+  float M = -__builtin_inff(), D = 0.f, A = 0.f;
+  for (int i0 = part; i0 < n; i0 += kMergeParts * kMergeUnroll) {
+    float mv[kMergeUnroll], lv[kMergeUnroll], av[kMergeUnroll];
+#pragma unroll
+    for (int u = 0; u < kMergeUnroll; ++u) {
+      const int i = i0 + kMergeParts * u;
+      const float* r = base + (size_t)min(i, n - 1) * step;
+      mv[u] = r[0];
+      lv[u] = r[1];
+      av[u] = r[4 + c];
+    }
+    // i < n is the same for every thread of a wave (two waves per part)
+    float mx = M;
+#pragma unroll
+    for (int u = 0; u < kMergeUnroll; ++u)
+      if (i0 + kMergeParts * u < n) mx = fmaxf(mx, mv[u]);
+    const float f = __builtin_amdgcn_exp2f(M - mx);  // M = -inf on the first batch: f = 0
+    D *= f;
+    A *= f;
+#pragma unroll
+    for (int u = 0; u < kMergeUnroll; ++u)
+      if (i0 + kMergeParts * u < n) {
+        const float w = __builtin_amdgcn_exp2f(mv[u] - mx);
+        D = fmaf(w, lv[u], D);
+        A = fmaf(w, av[u], A);
+      }
+    M = mx;
   }
-  mx = block_reduce(mx, true, scratch);
-  float den = 0.f;
-  for (int i = tid; i < n; i += kMergeThreads) {
-    const float f = __builtin_amdgcn_exp2f(wts[i] - mx);
-    wts[i] = f;
-    den = fmaf(f, base[i * step + 1], den);
+  if (c == 0) {
+    sm[part] = M;
+    sl[part] = D;
   }
-  den = block_reduce(den, false, scratch);  // also orders the wts writes before the reads below
-  const int c = tid & (kHeadDim - 1), half = tid >> 7;
-  float num = 0.f;
-#pragma unroll 8
-  for (int i = half; i < n; i += 2) num = fmaf(wts[i], base[i * step + 4 + c], num);
-  part[half][c] = num;
+  sa[part][c] = A;
   __syncthreads();
-  if (tid < kHeadDim) o[tid] = (part[0][tid] + part[1][tid]) / den;
+  if (tid < kHeadDim) {
+    float mx = sm[0];
+#pragma unroll
+    for (int p = 1; p < kMergeParts; ++p) mx = fmaxf(mx, sm[p]);
+    float den = 0.f, num = 0.f;
+#pragma unroll
+    for (int p = 0; p < kMergeParts; ++p) {
+      const float w = __builtin_amdgcn_exp2f(sm[p] - mx);  // a part without splits has sm = -inf: w = 0
+      den = fmaf(w, sl[p], den);
+      num = fmaf(w, sa[p][c], num);
+    }
+    o[c] = num / den;
+  }
 }
 
 template <int BK, int BV, int GQ>

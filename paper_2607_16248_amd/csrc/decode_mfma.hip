@@ -23,13 +23,15 @@
 //     holds p for the 8 tokens its B fragment needs (no transpose); output
 //     columns whose group differs from the channel's are discarded.
 //
-// Packed bits become operands with one AND per element pair: a set bit at
-// mantissa position w of a half is the exact fp16 subnormal 2^(w - 24).
-// The key-side weights 2^w depend only on the channel and are folded into
-// q~ once per decode; the value-side weights are split into a per-token-pair
-// part folded into the value scales and a per-channel-block part applied to
-// the accumulators at the end; the common 2^-24 goes into the fp32 scales.
-// The layouts that place the bits are in kvq_layout.h.
+// Packed bits become operands with one shift per 4-element block and one
+// AND per element pair: a set bit at mantissa position w of a half is the
+// exact fp16 subnormal 2^(w - 24), and the shift puts every bit among the
+// top mantissa positions, where the matrix cores keep the products of such
+// subnormals to near fp32 precision (see unpack8).  Element pair i of a
+// block weighs 2^i: on the key side this weight depends only on the channel
+// and is folded into q~ once per decode; on the value side it is the token
+// pair and is folded into the value scales; the common 2^(B0 - 24) goes into
+// the fp32 scales.  The layouts that place the bits are in kvq_layout.h.
 #include <hip/hip_runtime.h>
 
 #include "decode_common.h"
@@ -52,18 +54,24 @@ constexpr int kQRow = 80;  // dwords per Q' row in LDS: 64 + 16 of padding again
 __device__ __forceinline__ h2_t u2h(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
 __device__ __forceinline__ uint32_t h2u(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
 
-// One MFMA operand (8 halves) from the bits of 4-channel block blk4 in x
-// (bit plane `plane`): element pair i sits at bits (s, s + 16) with
-// s = pair_bit(blk4, 2i), and a single AND leaves each half equal to
-// bit * 2^(w - 24), an exact fp16 subnormal, with weight
-// w = 4*(blk4 & 1) + i + plane.  The other operand or the output carries
-// the inverse weight, so no multiply per element is needed.
+// One MFMA operand (8 halves) from the bits of 4-element block blk4 in x
+// (bit plane `plane` of a B-bit code): element pair i sits at bits
+// (s, s + 16), s = pair_bit(blk4, 2i) = 4*blk4 + i.  One shift moves the
+// block to mantissa positions B0 + plane + i with B0 = 7 - B, and one AND per
+// pair leaves each half equal to bit * 2^(B0 + plane + i - 24), an exact fp16
+// subnormal whose set bit is among the top mantissa bits 5..9.  (The matrix
+// cores add the products of subnormal fp16 inputs to about 2^-(13 + p)
+// relative precision for a set bit at mantissa position p; at 5..9 that is
+// 2^-18 or better.)  The other operand or the output carries 2^-i and
+// 2^(24 - B0); 2^plane is the bit's significance in the code.
+template <int B>
 __device__ __forceinline__ h8_t unpack8(uint32_t x, int blk4, int plane) {
-  const uint32_t src = blk4 < 2 ? (plane ? x << 1 : x) : (plane ? x >> 7 : x >> 8);
-  const int base = 4 * (blk4 & 1) + plane;
+  constexpr int kB0 = 7 - B;
+  const int sh = 4 * blk4 - kB0 - plane;
+  const uint32_t src = sh > 0 ? x >> sh : x << -sh;
   u4_t w;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (base + i));
+  for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (kB0 + plane + i));
   return __builtin_bit_cast(h8_t, w);
 }
 
@@ -201,10 +209,32 @@ decode_mfma_kernel(DecodeArgs a) {
   lo.vs = (gsel * 32 + 8 * row) * 2;
   lo.vz = lo.vs + ng * 64;
 
+  // This wave's 32-token blocks: key groups j0 + wv + kWaves*n, each of
+  // BPG blocks; block i is key group j0 + kWaves*(i / BPG), part i % BPG.
+  const int t0 = wk.sp * a.split_tokens;
+  const int t1 = min(S.Lq, t0 + a.split_tokens);
+  const int j0 = t0 / a.gk + wv, jend = t1 / a.gk;
+  const int ngroups = j0 < jend ? (jend - j0 + kWaves - 1) / kWaves : 0;
+  const int nblocks = ngroups * BPG;
+  const int last = nblocks - 1;
+  const int vstride = 128 * ng;
+  auto load = [&](int i, BlockData<BK, BV>& o) {
+    const int j = j0 + kWaves * (i / BPG);
+    const int tok = j * a.gk + (i % BPG) * 32;
+    load_block<BK, BV>(rs, lo, a.km + (uint32_t)j * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
+                       a.vc + (uint32_t)(tok / 32) * 512 * BV, a.vm + (uint32_t)(tok / 32) * vstride, o);
+  };
+  // the first two blocks load while the query is prepared
+  BlockData<BK, BV> b0, b1, b2;
+  if (nblocks > 0) {
+    load(0, b0);
+    load(min(1, last), b1);
+  }
+
   // q~ = q * 2^-e per head with max |q~| < 1.  For the code MFMA each lane's
   // channel pair (2*lane, 2*lane+1) also carries 2^-w, w = the bit weight of
   // those channels in the unpacked key operand.
-  const float wq = ldexpf(1.f, -(4 * ((lane >> 4) & 1) + (lane & 3)));
+  const float wq = ldexpf(1.f, -(lane & 3));
   uint32_t qt[kGQ];
   float inv[kGQ], csc[kGQ];
 #pragma unroll
@@ -215,7 +245,7 @@ decode_mfma_kernel(DecodeArgs a) {
     int e = 0;
     frexpf(mx, &e);
     inv[g] = ldexpf(1.f, -e);
-    csc[g] = ldexpf(a.qscale, e + 24);  // undoes 2^-e and the 2^-24 of the code operand
+    csc[g] = ldexpf(a.qscale, e + 24 - (7 - BK));  // undoes 2^-e and the code operand's 2^(B0 - 24)
     h2_t t;
     t.x = (_Float16)(q0 * inv[g] * wq);
     t.y = (_Float16)(q1 * inv[g] * wq);
@@ -242,15 +272,7 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
   for (int mb = 0; mb < 8; ++mb) acc[mb] = (f4_t){0.f, 0.f, 0.f, 0.f};
 
-  const int t0 = wk.sp * a.split_tokens;
-  const int t1 = min(S.Lq, t0 + a.split_tokens);
   uint32_t* ql = q_lds[wv];
-
-  // This wave's 32-token blocks: key groups j0 + wv + kWaves*n, each of
-  // BPG blocks.
-  const int j0 = t0 / a.gk + wv, jend = t1 / a.gk;
-  const int ngroups = j0 < jend ? (jend - j0 + kWaves - 1) / kWaves : 0;
-  const int nblocks = ngroups * BPG;
 
   // lanes whose quad member index has bit 0 / bit 1 set
   const bool xb0 = xc & 1, xb1 = xc & 2;
@@ -281,7 +303,7 @@ decode_mfma_kernel(DecodeArgs a) {
       dz = (f4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) dz = mfma(az[kb], bq[kb], dz);
-      dz *= 0x1p-24f;  // to the scale of the code products
+      dz *= ldexpf(1.f, (7 - BK) - 24);  // to the scale of the code products
     }
 
     // unscaled scores (hi + lo) of tokens t = 4*mb + e, token 16*mb + 4*row + e
@@ -292,7 +314,7 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int p = 0; p < BK; ++p) d[mb] = mfma(unpack8(cur.kx[mb][p], kb, p), bp[kb], d[mb]);
+        for (int p = 0; p < BK; ++p) d[mb] = mfma(unpack8<BK>(cur.kx[mb][p], kb, p), bp[kb], d[mb]);
     }
     float raw[8];
 #pragma unroll
@@ -336,11 +358,11 @@ decode_mfma_kernel(DecodeArgs a) {
       const h2_t s2 = t == 0 ? u2h(cur.sv[t])
                              : u2h(cur.sv[t]) * (h2_t){(_Float16)(1.f / (1 << t)), (_Float16)(1.f / (1 << t))};
       const float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
-      const h2_t hi = __builtin_bit_cast(h2_t, __builtin_amdgcn_cvt_pkrtz(f0, f1));
+      const h2_t hi = (h2_t){(_Float16)f0, (_Float16)f1};  // nearest: the residuals carry both signs
       const float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
       const float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
       bhi[t] = h2u(hi);
-      blo[t] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(g0, g1));
+      blo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
       const h2_t z2 = u2h(cur.zv[t]);
       zacc = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc));
     }
@@ -349,19 +371,11 @@ decode_mfma_kernel(DecodeArgs a) {
     for (int mb = 0; mb < 8; ++mb) {
 #pragma unroll
       for (int p2 = 0; p2 < BV; ++p2) {
-        const h8_t av = unpack8(cur.vx[(mb >> 2) * BV + p2], mb & 3, p2);
+        const h8_t av = unpack8<BV>(cur.vx[(mb >> 2) * BV + p2], mb & 3, p2);
         acc[mb] = mfma(av, BH, acc[mb]);
         acc[mb] = mfma(av, BL, acc[mb]);
       }
     }
-  };
-  // block i of this wave: key group j0 + kWaves*(i / BPG), 32-token part i % BPG
-  const int vstride = 128 * ng;
-  auto load = [&](int i, BlockData<BK, BV>& o) {
-    const int j = j0 + kWaves * (i / BPG);
-    const int tok = j * a.gk + (i % BPG) * 32;
-    load_block<BK, BV>(rs, lo, a.km + (uint32_t)j * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
-                       a.vc + (uint32_t)(tok / 32) * 512 * BV, a.vm + (uint32_t)(tok / 32) * vstride, o);
   };
 
   // Three buffers, loads two blocks ahead of the arithmetic.  The loads are
@@ -370,10 +384,6 @@ decode_mfma_kernel(DecodeArgs a) {
   // exact; the main loop has no early exit, the last one or two blocks run
   // after it.
   if (nblocks > 0) {
-    const int last = nblocks - 1;
-    BlockData<BK, BV> b0, b1, b2;
-    load(0, b0);
-    load(min(1, last), b1);
     int i = 0;
     for (; i + 3 <= nblocks; i += 3) {
       load(min(i + 2, last), b2);
@@ -399,8 +409,8 @@ decode_mfma_kernel(DecodeArgs a) {
   for (int mb = 0; mb < 8; ++mb) {
     if (xc == (16 * mb) / a.gv) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e)  // undo the channel block's bit weight 2^(4*(mb & 1)) and the 2^-24
-        red.acc[wv][hc * kHeadDim + 16 * mb + 4 * row + e] = fmaf(acc[mb][e], (mb & 1) ? 0x1p20f : 0x1p24f, zacc);
+      for (int e = 0; e < 4; ++e)  // undo the code operand's 2^(B0 - 24)
+        red.acc[wv][hc * kHeadDim + 16 * mb + 4 * row + e] = fmaf(acc[mb][e], ldexpf(1.f, 24 - (7 - BV)), zacc);
     }
   }
   if (row == 0 && xc == 0) {
