@@ -49,6 +49,9 @@ typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kGQ = 4;
+// Headroom of the softmax reference above the largest score seen (log2
+// units): weights of later tokens within it need no rescale.
+constexpr float kLazyMargin = 3.f;
 constexpr int kQRow = 80;  // dwords per Q' row in LDS: 64 + 16 of padding against bank conflicts
 
 __device__ __forceinline__ h2_t u2h(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
@@ -323,30 +326,34 @@ decode_mfma_kernel(DecodeArgs a) {
       for (int e = 0; e < 4; ++e) raw[4 * mb + e] = d[mb][e] + dpp_mov<kQuadXor1>(0.f, d[mb][e]);
 
     // online softmax (base 2) for head hc over these 32 tokens; cs > 0, so
-    // the maximum is taken before scaling
+    // the maximum is taken before scaling.  The reference m moves only when a
+    // score exceeds it, and then to kLazyMargin above that score: every
+    // weight stays <= 1, and the rescale of the accumulators (and its
+    // exponential) is skipped while later maxima stay under the reference.
     float bm = fmaxf(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])),
                      fmaxf(fmaxf(raw[4], raw[5]), fmaxf(raw[6], raw[7])));
     bm = max_across_rows(bm) * cs;
-    const float mnew = fmaxf(m, bm);
-    const float alpha = __builtin_amdgcn_exp2f(m - mnew);
-    m = mnew;
+    if (__builtin_amdgcn_ballot_w64(bm > m)) {
+      const float mnew = bm > m ? bm + kLazyMargin : m;
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);  // 1 where the reference stays
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) acc[mb] *= alpha;
+      zacc *= alpha;
+      l *= alpha;
+      m = mnew;
+    }
     // the four lanes of a quad hold the same eight scores: member k takes
     // the exponentials of token pair k, then every member gets all eight
     const float r0 = xb1 ? (xb0 ? raw[6] : raw[4]) : (xb0 ? raw[2] : raw[0]);
     const float r1 = xb1 ? (xb0 ? raw[7] : raw[5]) : (xb0 ? raw[3] : raw[1]);
-    const float e0 = __builtin_amdgcn_exp2f(fmaf(r0, cs, -mnew));
-    const float e1 = __builtin_amdgcn_exp2f(fmaf(r1, cs, -mnew));
-    l = fmaf(l, alpha, e0 + e1);
+    const float e0 = __builtin_amdgcn_exp2f(fmaf(r0, cs, -m));
+    const float e1 = __builtin_amdgcn_exp2f(fmaf(r1, cs, -m));
+    l += e0 + e1;
     float p[8];
     p[0] = quad_bcast<0>(e0); p[1] = quad_bcast<0>(e1);
     p[2] = quad_bcast<1>(e0); p[3] = quad_bcast<1>(e1);
     p[4] = quad_bcast<2>(e0); p[5] = quad_bcast<2>(e1);
     p[6] = quad_bcast<3>(e0); p[7] = quad_bcast<3>(e1);
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb) acc[mb] *= alpha;
-      zacc *= alpha;
-    }
 
     // P' = p * s_v as fp16 hi + lo: the product and its residual are each
     // one mixed-precision fma from the fp32 p and the fp16 scale; element
