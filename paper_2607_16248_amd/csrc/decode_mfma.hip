@@ -8,20 +8,22 @@
 // the vector ALUs can retire at HBM speed, so both contractions go to the
 // matrix cores with every product exact and fp32 accumulation:
 //
-//   scores:  S^T[t][col] = sum_c code[t][c] * Q'[c][col] + sum_c z[c] * q~[c]
-//     A = key codes as exact fp16 0/1 (or 0/2 for the high bit plane),
-//     B = Q' = q~ (.) s split into fp16 hi + lo parts (two product terms,
+//   scores:  S[row][t] = sum_c Q'[row][c] * code[t][c] + sum_c q~[row][c] * z[c]
+//     A = Q' = q~ (.) s split into fp16 hi + lo parts (two product terms,
 //         each exact: q~ and s are fp16, their product fits two halves),
-//     column col = 4*head + x: x = 0, 2 carry hi, x = 1, 3 carry lo; adding
-//     the neighbour column gives hi + lo in every lane of the head.
-//     The zero-point term uses A = z broadcast over tokens and B = q~.
-//     q~ = q * 2^-e with |q~| < 1 keeps every fp16 operand finite; the scale
-//     2^e * log2(e) / sqrt(d) is applied to the fp32 result.
+//         row = 4*head + x: x = 0, 2 carry hi, x = 1, 3 carry lo,
+//     B = key codes as exact fp16 0/1 (or 0/2 for the high bit plane).
+//     A lane of the result holds one token of one head (elements x), so
+//     every lane takes its own exponentials and a 16-lane row reduces the
+//     block maximum of its head.  The zero-point term uses A = q~ and B = z
+//     broadcast over tokens.  q~ = q * 2^-e with |q~| < 1 keeps every fp16
+//     operand finite; the scale 2^e * log2(e) / sqrt(d) is applied to the
+//     fp32 result.
 //   values:  O^T[c][col] = sum_t code[t][c] * P'[t][col] (+ z term on VALU)
 //     A = value codes (exact fp16), B = P' = p * s_v split hi / lo,
-//     column col = 4*head + value group: a lane of the score layout already
-//     holds p for the 8 tokens its B fragment needs (no transpose); output
-//     columns whose group differs from the channel's are discarded.
+//     column col = 4*head + value group; the weights p reach the B layout
+//     through 512 bytes of LDS per wave; output columns whose group differs
+//     from the channel's are discarded.
 //
 // Packed bits become operands with one shift per 4-element block and one
 // AND per element pair: a set bit at mantissa position w of a half is the
@@ -30,7 +32,7 @@
 // subnormals to near fp32 precision (see unpack8).  Element pair i of a
 // block weighs 2^i: on the key side this weight depends only on the channel
 // and is folded into q~ once per decode; on the value side it is the token
-// pair and is folded into the value scales; the common 2^(B0 - 24) goes into
+// pair and is folded into the weights p; the common 2^(B0 - 24) goes into
 // the fp32 scales.  The layouts that place the bits are in kvq_layout.h.
 #include <hip/hip_runtime.h>
 
@@ -52,7 +54,12 @@ constexpr int kGQ = 4;
 // Headroom of the softmax reference above the largest score seen (log2
 // units): weights of later tokens within it need no rescale.
 constexpr float kLazyMargin = 3.f;
-constexpr int kQRow = 80;  // dwords per Q' row in LDS: 64 + 16 of padding against bank conflicts
+// dwords per Q' row in LDS: 64 + 4 of padding, so that the eight rows one
+// 8-lane group of a 16-byte read touches start in different bank quads
+constexpr int kQRow = 68;
+// floats per head row of the weights handed from the score to the value
+// layout: 32 + 16 of padding (rows 2r and 2r+1 fall in different bank halves)
+constexpr int kPRow = 48;
 
 __device__ __forceinline__ h2_t u2h(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
 __device__ __forceinline__ uint32_t h2u(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
@@ -168,18 +175,21 @@ __device__ __forceinline__ float quad_bcast(float v) {
 }
 
 // Waves per SIMD the instantiation is compiled for: three where its
-// registers fit 168 without spilling, else two.
+// registers fit 168 without spilling (one 32-token block per key group),
+// else two.
 template <int BK, int BV, int BPG>
 struct MatrixOcc {
-  static constexpr int value = (BK + BV <= 3 && BK * BV * BPG <= 2) ? 3 : 2;
+  static constexpr int value = BPG == 1 ? 3 : 2;
 };
 
 template <int BK, int BV, int BPG>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MatrixOcc<BK, BV, BPG>::value))) void
 decode_mfma_kernel(DecodeArgs a) {
-  __shared__ uint32_t q_lds[kWaves][(2 * kGQ + 1) * kQRow];  // Q' hi rows, lo rows, key zero-points
-  __shared__ float qp_lds[kWaves][kHeadDim * kGQ];  // fp16 tail split only
-  __shared__ float p_lds[kWaves][32 * kGQ];         // fp16 tail split only
+  // per wave: Q' hi rows, lo rows, the key zero-points, then q~ rows and a zero row
+  // (16-byte aligned: rows are read with 16-byte loads)
+  __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * kGQ + 2) * kQRow];
+  __shared__ float qp_lds[kWaves][kHeadDim * kGQ];                          // fp16 tail split only
+  __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * kGQ];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<kGQ> red;
 
   const Work wk = find_work(a);
@@ -238,6 +248,8 @@ decode_mfma_kernel(DecodeArgs a) {
   // channel pair (2*lane, 2*lane+1) also carries 2^-w, w = the bit weight of
   // those channels in the unpacked key operand.
   const float wq = ldexpf(1.f, -(lane & 3));
+  uint32_t* ql = q_lds[wv];
+  uint32_t* qq = ql + (2 * kGQ + 1) * kQRow;  // q~ of head g in row g, zeros in row kGQ
   uint32_t qt[kGQ];
   float inv[kGQ], csc[kGQ];
 #pragma unroll
@@ -253,32 +265,27 @@ decode_mfma_kernel(DecodeArgs a) {
     t.x = (_Float16)(q0 * inv[g] * wq);
     t.y = (_Float16)(q1 * inv[g] * wq);
     qt[g] = h2u(t);
+    qq[g * kQRow + lane] = h2u((h2_t){(_Float16)(q0 * inv[g]), (_Float16)(q1 * inv[g])});
   }
-  const float cs = pick4(csc, hc);
+  qq[kGQ * kQRow + lane] = 0u;
+  // score layout: token col of the 16-token tile, head row
+  const float cs = pick4(csc, row);
 
-  // B operand of the zero-point term: column (hc, hi) holds q~ of head hc
-  h8_t bq[4];
-  {
-    const float iv = pick4(inv, hc);
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      const h8_t raw = *reinterpret_cast<const h8_t*>(qrow + hc * kHeadDim + 32 * kb + 8 * row);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) bq[kb][e] = part ? (_Float16)0.f : (_Float16)((float)raw[e] * iv);
-    }
-  }
+  // A-operand row of the zero-point term: q~ of head hc in the hi rows, zeros in the lo rows
+  const uint32_t* qqrow = qq + (part ? kGQ : hc) * kQRow + 4 * row;
 
-  // m, l: running maximum and denominator (l holds this lane's own token
-  // pairs only); zacc: the value zero-point term of the lane's group
-  float m = -__builtin_inff(), l = 0.f, zacc = 0.f;
+  // Score layout: m = the softmax reference of head row (uniform over the
+  // row), mo0 / mo1 = m plus the pair weights ta, ta + 2 of the lane's two
+  // tokens (see the rescale below), l = the sum of the lane's own weights
+  // times 2^-ta.  Value layout:
+  // zacc[t] = the zero-point term of element pair t of the lane's group.
+  float m = -__builtin_inff(), mo0 = 0.f, mo1 = 0.f, l = 0.f;
+  float zacc[4] = {0.f, 0.f, 0.f, 0.f};
   f4_t acc[8];
 #pragma unroll
   for (int mb = 0; mb < 8; ++mb) acc[mb] = (f4_t){0.f, 0.f, 0.f, 0.f};
 
-  uint32_t* ql = q_lds[wv];
-
-  // lanes whose quad member index has bit 0 / bit 1 set
-  const bool xb0 = xc & 1, xb1 = xc & 2;
+  float* pl = p_lds[wv];
 
   f4_t dz = {0.f, 0.f, 0.f, 0.f};
   h8_t bp[4];
@@ -297,19 +304,20 @@ decode_mfma_kernel(DecodeArgs a) {
       }
       ql[2 * kGQ * kQRow + lane] = cur.z;
       wave_lds_sync();
-      h8_t az[4];
+      h8_t az[4], aq[4];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         bp[kb] = *reinterpret_cast<const h8_t*>(&ql[(part * kGQ + hc) * kQRow + 16 * kb + 4 * row]);
         az[kb] = *reinterpret_cast<const h8_t*>(&ql[2 * kGQ * kQRow + 16 * kb + 4 * row]);
+        aq[kb] = *reinterpret_cast<const h8_t*>(&qqrow[16 * kb]);
       }
       dz = (f4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) dz = mfma(az[kb], bq[kb], dz);
-      dz *= ldexpf(1.f, (7 - BK) - 24);  // to the scale of the code products
+      for (int kb = 0; kb < 4; ++kb) dz = mfma(aq[kb], az[kb], dz);
+      dz[0] *= ldexpf(1.f, (7 - BK) - 24);  // to the scale of the code products (hi row)
     }
 
-    // unscaled scores (hi + lo) of tokens t = 4*mb + e, token 16*mb + 4*row + e
+    // unscaled scores of token 16*mb + col for head row: hi + lo rows
     f4_t d[2];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
@@ -317,53 +325,57 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int p = 0; p < BK; ++p) d[mb] = mfma(unpack8<BK>(cur.kx[mb][p], kb, p), bp[kb], d[mb]);
+        for (int p = 0; p < BK; ++p) d[mb] = mfma(bp[kb], unpack8<BK>(cur.kx[mb][p], kb, p), d[mb]);
     }
-    float raw[8];
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) raw[4 * mb + e] = d[mb][e] + dpp_mov<kQuadXor1>(0.f, d[mb][e]);
+    const float raw0 = d[0][0] + d[0][1], raw1 = d[1][0] + d[1][1];
 
-    // online softmax (base 2) for head hc over these 32 tokens; cs > 0, so
+    // online softmax (base 2) for head row over these 32 tokens; cs > 0, so
     // the maximum is taken before scaling.  The reference m moves only when a
     // score exceeds it, and then to kLazyMargin above that score: every
     // weight stays <= 1, and the rescale of the accumulators (and its
     // exponential) is skipped while later maxima stay under the reference.
-    float bm = fmaxf(fmaxf(fmaxf(raw[0], raw[1]), fmaxf(raw[2], raw[3])),
-                     fmaxf(fmaxf(raw[4], raw[5]), fmaxf(raw[6], raw[7])));
-    bm = max_across_rows(bm) * cs;
+    const float ninf = -__builtin_inff();
+    float bm = fmaxf(raw0, raw1);
+    bm = fmaxf(bm, dpp_mov<kQuadXor1>(ninf, bm));
+    bm = fmaxf(bm, dpp_mov<kQuadXor2>(ninf, bm));
+    bm = fmaxf(bm, dpp_mov<kHalfMirror>(ninf, bm));
+    bm = fmaxf(bm, dpp_mov<kMirror>(ninf, bm));
+    bm *= cs;
     if (__builtin_amdgcn_ballot_w64(bm > m)) {
       const float mnew = bm > m ? bm + kLazyMargin : m;
       const float alpha = __builtin_amdgcn_exp2f(m - mnew);  // 1 where the reference stays
-#pragma unroll
-      for (int mb = 0; mb < 8; ++mb) acc[mb] *= alpha;
-      zacc *= alpha;
       l *= alpha;
       m = mnew;
+      // the value operand's element pair of this lane's token of tile 0 is
+      // ta = (col >> 1) & 1 (tile 1: ta + 2); its weight 2^-ta goes into p
+      mo0 = m + (float)((__lane_id() >> 1) & 1);
+      mo1 = mo0 + 2.f;
+      const float av = __shfl(alpha, 16 * hc);  // the same factor in the value layout
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) acc[mb] *= av;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) zacc[t] *= av;
     }
-    // the four lanes of a quad hold the same eight scores: member k takes
-    // the exponentials of token pair k, then every member gets all eight
-    const float r0 = xb1 ? (xb0 ? raw[6] : raw[4]) : (xb0 ? raw[2] : raw[0]);
-    const float r1 = xb1 ? (xb0 ? raw[7] : raw[5]) : (xb0 ? raw[3] : raw[1]);
-    const float e0 = __builtin_amdgcn_exp2f(fmaf(r0, cs, -m));
-    const float e1 = __builtin_amdgcn_exp2f(fmaf(r1, cs, -m));
-    l += e0 + e1;
-    float p[8];
-    p[0] = quad_bcast<0>(e0); p[1] = quad_bcast<0>(e1);
-    p[2] = quad_bcast<1>(e0); p[3] = quad_bcast<1>(e1);
-    p[4] = quad_bcast<2>(e0); p[5] = quad_bcast<2>(e1);
-    p[6] = quad_bcast<3>(e0); p[7] = quad_bcast<3>(e1);
+    // p * 2^-t for the lane's two tokens (element pairs ta and ta + 2)
+    const float e0 = __builtin_amdgcn_exp2f(fmaf(raw0, cs, -mo0));
+    const float e1 = __builtin_amdgcn_exp2f(fmaf(raw1, cs, -mo1));
+    l += fmaf(e1, 4.f, e0);
+    // to the value layout: lane (col, row) needs tokens 4*row + 0..3 and
+    // 16 + 4*row + 0..3 of head hc
+    wave_lds_sync();
+    pl[row * kPRow + col] = e0;
+    pl[row * kPRow + 16 + col] = e1;
+    wave_lds_sync();
+    const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[hc * kPRow + 4 * row]);
+    const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[hc * kPRow + 16 + 4 * row]);
+    const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
 
     // P' = p * s_v as fp16 hi + lo: the product and its residual are each
-    // one mixed-precision fma from the fp32 p and the fp16 scale; element
-    // pair t also carries 2^-t, the inverse of its bit weight in the
-    // unpacked value operand
+    // one mixed-precision fma from the fp32 p and the fp16 scale
     u4_t bhi, blo;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const h2_t s2 = t == 0 ? u2h(cur.sv[t])
-                             : u2h(cur.sv[t]) * (h2_t){(_Float16)(1.f / (1 << t)), (_Float16)(1.f / (1 << t))};
+      const h2_t s2 = u2h(cur.sv[t]);
       const float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
       const h2_t hi = (h2_t){(_Float16)f0, (_Float16)f1};  // nearest: the residuals carry both signs
       const float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
@@ -371,7 +383,7 @@ decode_mfma_kernel(DecodeArgs a) {
       bhi[t] = h2u(hi);
       blo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
       const h2_t z2 = u2h(cur.zv[t]);
-      zacc = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc));
+      zacc[t] = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc[t]));
     }
     const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
 #pragma unroll
@@ -404,25 +416,31 @@ decode_mfma_kernel(DecodeArgs a) {
     if (i + 1 < nblocks) process(b1, i + 1);
   }
 
-  // sums over the quad (l holds own token pairs) and over the lane rows;
-  // the lanes of one head then agree on m and l
+  // Lane coordinates again, from the lane id: recomputing them here keeps
+  // the loop's register budget free of epilogue-only values.
+  const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const int ecol = ln & 15, erow = ln >> 4, ehc = ecol >> 2, exc = ecol & 3;
+  // l: undo 2^-ta and sum the 16 lanes of the head's row; zacc: undo the
+  // pair weights and sum over the lane rows (the tokens of a group column)
+  l = ldexpf(l, (ecol >> 1) & 1);
   l += dpp_mov<kQuadXor1>(0.f, l);
   l += dpp_mov<kQuadXor2>(0.f, l);
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-  zacc += __shfl_xor(zacc, 16);
-  zacc += __shfl_xor(zacc, 32);
+  l += dpp_mov<kHalfMirror>(0.f, l);
+  l += dpp_mov<kMirror>(0.f, l);
+  float zs = fmaf(zacc[3], 8.f, fmaf(zacc[2], 4.f, fmaf(zacc[1], 2.f, zacc[0])));
+  zs += __shfl_xor(zs, 16);
+  zs += __shfl_xor(zs, 32);
 #pragma unroll
   for (int mb = 0; mb < 8; ++mb) {
-    if (xc == (16 * mb) / a.gv) {
+    if (exc == (16 * mb) / a.gv) {
 #pragma unroll
       for (int e = 0; e < 4; ++e)  // undo the code operand's 2^(B0 - 24)
-        red.acc[wv][hc * kHeadDim + 16 * mb + 4 * row + e] = fmaf(acc[mb][e], ldexpf(1.f, 24 - (7 - BV)), zacc);
+        red.acc[wv][ehc * kHeadDim + 16 * mb + 4 * erow + e] = fmaf(acc[mb][e], ldexpf(1.f, 24 - (7 - BV)), zs);
     }
   }
-  if (row == 0 && xc == 0) {
-    red.m[wv][hc] = m;
-    red.l[wv][hc] = l;
+  if (ecol == 0) {
+    red.m[wv][erow] = m;
+    red.l[wv][erow] = l;
   }
   __syncthreads();
   write_record<kGQ>(a, S, wk.h, wk.sp, red);

@@ -122,12 +122,17 @@ HeadLayout layout_of(const kvq_cache_desc* d, int bk, int bv) {
 int32_t split_tokens_for(const kvq_cache* c) {
   const int gk = c->d.key_group;
   if (c->split_tokens > 0) return c->split_tokens;
-  int64_t total = 0, lq_max = 0;
+  int64_t total = 0, lq_max = 0, tails = 0;
   for (int i = 0; i < c->d.batch; ++i) {
     total += (int64_t)c->Lq[i] * c->d.num_kv_heads;
     lq_max = std::max<int64_t>(lq_max, c->Lq[i]);
+    if (c->L[i] > c->Lq[i]) tails += c->d.num_kv_heads;
   }
-  const int64_t target = target_workgroups(c->occupancy);
+  // The fp16-tail workgroups (one per sequence and kv head with tail tokens)
+  // share the same round of resident workgroups: a workgroup that has to
+  // wait for a free slot would add a whole split's time to the launch.
+  const int64_t target = std::max<int64_t>(target_workgroups(c->occupancy) - tails,
+                                           target_workgroups(c->occupancy) / 2);
   int64_t st = (total + target - 1) / target;
   st = std::max<int64_t>(st, (lq_max + kMaxSplits - 1) / kMaxSplits);
   st = (st + gk - 1) / gk * gk;
