@@ -60,6 +60,10 @@ constexpr int kQRow = 68;
 // floats per head row of the weights handed from the score to the value
 // layout: 32 + 16 of padding (rows 2r and 2r+1 fall in different bank halves)
 constexpr int kPRow = 48;
+// Blocks per zero-point table (a multiple of the main loop's unroll of 3):
+// the table holds the zero-point terms of the kChunk / BPG key groups a wave
+// processes next.
+constexpr int kChunk = 48;
 
 __device__ __forceinline__ h2_t u2h(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
 __device__ __forceinline__ uint32_t h2u(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
@@ -129,7 +133,6 @@ __device__ __forceinline__ u4_t ld128(__amdgpu_buffer_rsrc_t r, uint32_t v, uint
 template <int BK, int BV>
 struct BlockData {
   uint32_t s;          // key scales of channels 2*lane, 2*lane+1 (this block's key group)
-  uint32_t z;          // key zero-points of the same channels
   uint32_t kx[2][BK];  // key codes of tokens 16*mb + (lane & 15)
   uint32_t vx[2 * BV]; // value codes of this lane
   u4_t sv, zv;         // value scales / zeros of this lane's 8 tokens and group, element order
@@ -144,7 +147,6 @@ template <int BK, int BV>
 __device__ __forceinline__ void load_block(__amdgpu_buffer_rsrc_t r, const LaneOffsets& lo, uint32_t km,
                                            uint32_t kc, uint32_t vc, uint32_t vm, BlockData<BK, BV>& o) {
   o.s = ld32(r, lo.km, km);
-  o.z = ld32(r, lo.km + kHeadDim * 2, km);
 #pragma unroll
   for (int mb = 0; mb < 2; ++mb) {
     if constexpr (BK == 1) {
@@ -185,9 +187,10 @@ struct MatrixOcc {
 template <int BK, int BV, int BPG>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MatrixOcc<BK, BV, BPG>::value))) void
 decode_mfma_kernel(DecodeArgs a) {
-  // per wave: Q' hi rows, lo rows, the key zero-points, then q~ rows and a zero row
-  // (16-byte aligned: rows are read with 16-byte loads)
-  __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * kGQ + 2) * kQRow];
+  // per wave: Q' hi rows, lo rows, q~ rows, then the zero-point terms of up
+  // to kChunk key groups (16-byte aligned: rows are read with 16-byte loads)
+  static_assert(kChunk * kGQ <= 3 * kQRow, "zero-point table rows");
+  __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * kGQ + 3) * kQRow];
   __shared__ float qp_lds[kWaves][kHeadDim * kGQ];                          // fp16 tail split only
   __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * kGQ];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<kGQ> red;
@@ -237,11 +240,21 @@ decode_mfma_kernel(DecodeArgs a) {
     load_block<BK, BV>(rs, lo, a.km + (uint32_t)j * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
                        a.vc + (uint32_t)(tok / 32) * 512 * BV, a.vm + (uint32_t)(tok / 32) * vstride, o);
   };
-  // the first two blocks load while the query is prepared
+  // Key zero-points of the wave's key groups k0 .. k0 + 15 as the A operand
+  // of their zero-point terms (row = group; past the last group: the last).
+  auto load_z = [&](int k0, h8_t (&zq)[4]) {
+    const uint32_t j = (uint32_t)(j0 + kWaves * min(k0 + col, ngroups - 1));
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      zq[kb] = __builtin_bit_cast(h8_t, ld128(rs, j * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
+  };
+  // the first two blocks and the first zero-points load while the query is prepared
   BlockData<BK, BV> b0, b1, b2;
+  h8_t zq[4];
   if (nblocks > 0) {
     load(0, b0);
     load(min(1, last), b1);
+    load_z(0, zq);
   }
 
   // q~ = q * 2^-e per head with max |q~| < 1.  For the code MFMA each lane's
@@ -249,7 +262,8 @@ decode_mfma_kernel(DecodeArgs a) {
   // those channels in the unpacked key operand.
   const float wq = ldexpf(1.f, -(lane & 3));
   uint32_t* ql = q_lds[wv];
-  uint32_t* qq = ql + (2 * kGQ + 1) * kQRow;  // q~ of head g in row g, zeros in row kGQ
+  uint32_t* qq = ql + 2 * kGQ * kQRow;  // q~ of head g in row g
+  float* dzt = reinterpret_cast<float*>(ql + 3 * kGQ * kQRow);  // [group k mod (kChunk / BPG)][head]
   uint32_t qt[kGQ];
   float inv[kGQ], csc[kGQ];
 #pragma unroll
@@ -267,12 +281,37 @@ decode_mfma_kernel(DecodeArgs a) {
     qt[g] = h2u(t);
     qq[g * kQRow + lane] = h2u((h2_t){(_Float16)(q0 * inv[g]), (_Float16)(q1 * inv[g])});
   }
-  qq[kGQ * kQRow + lane] = 0u;
   // score layout: token col of the 16-token tile, head row
   const float cs = pick4(csc, row);
 
-  // A-operand row of the zero-point term: q~ of head hc in the hi rows, zeros in the lo rows
-  const uint32_t* qqrow = qq + (part ? kGQ : hc) * kQRow + 4 * row;
+  // Zero-point terms sum_c z[c] q~[c] of 16 key groups and the 4 heads, in
+  // one MFMA chain (A = z of group col, B = q~ of head hc), scaled like the
+  // code products, into table rows s .. s + 15; lanes of column 4*head hold
+  // groups 4*row .. 4*row + 3.
+  auto dz_rows = [&](int s, const h8_t (&zq)[4]) {
+    f4_t t = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+      t = mfma(zq[kb], *reinterpret_cast<const h8_t*>(&qq[hc * kQRow + 16 * kb + 4 * row]), t);
+    if (xc == 0) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dzt[(s + 4 * row + e) * kGQ + hc] = t[e] * ldexpf(1.f, (7 - BK) - 24);
+    }
+  };
+  // The table for the wave's groups k0 .. k0 + kChunk / BPG - 1; zq holds
+  // the zero-points of the first 16 (the rest load here: only long splits
+  // have them).
+  constexpr int kChunkGroups = kChunk / BPG;
+  auto fill_table = [&](int k0, const h8_t (&zq)[4]) {
+    wave_lds_sync();  // the q~ rows are written, earlier reads of the table are done
+    dz_rows(0, zq);
+    for (int s = 16; s < kChunkGroups && k0 + s < ngroups; s += 16) {
+      h8_t zn[4];
+      load_z(k0 + s, zn);
+      dz_rows(s, zn);
+    }
+  };
+  if (nblocks > 0) fill_table(0, zq);
 
   // Score layout: m = the softmax reference of head row (uniform over the
   // row), mo0 / mo1 = m plus the pair weights ta, ta + 2 of the lane's two
@@ -291,8 +330,9 @@ decode_mfma_kernel(DecodeArgs a) {
   h8_t bp[4];
   auto process = [&](const BlockData<BK, BV>& cur, int i) {
     if (BPG == 1 || i % BPG == 0) {
-      // Q' = q~ (.) s of the block's key group, hi and lo halves, and the
-      // group's zero-points, re-laid out through LDS
+      const int k = i / BPG;  // the wave's key group
+      // Q' = q~ (.) s of the block's key group, hi and lo halves, re-laid
+      // out through LDS
       wave_lds_sync();
 #pragma unroll
       for (int g = 0; g < kGQ; ++g) {
@@ -302,19 +342,12 @@ decode_mfma_kernel(DecodeArgs a) {
         ql[g * kQRow + lane] = h2u(hi);
         ql[(kGQ + g) * kQRow + lane] = h2u(lo);
       }
-      ql[2 * kGQ * kQRow + lane] = cur.z;
       wave_lds_sync();
-      h8_t az[4], aq[4];
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
+      for (int kb = 0; kb < 4; ++kb)
         bp[kb] = *reinterpret_cast<const h8_t*>(&ql[(part * kGQ + hc) * kQRow + 16 * kb + 4 * row]);
-        az[kb] = *reinterpret_cast<const h8_t*>(&ql[2 * kGQ * kQRow + 16 * kb + 4 * row]);
-        aq[kb] = *reinterpret_cast<const h8_t*>(&qqrow[16 * kb]);
-      }
-      dz = (f4_t){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) dz = mfma(aq[kb], az[kb], dz);
-      dz[0] *= ldexpf(1.f, (7 - BK) - 24);  // to the scale of the code products (hi row)
+      // the group's zero-point term enters the hi row of the scores
+      dz = (f4_t){dzt[(k % kChunkGroups) * kGQ + row], 0.f, 0.f, 0.f};
     }
 
     // unscaled scores of token 16*mb + col for head row: hi + lo rows
@@ -402,15 +435,25 @@ decode_mfma_kernel(DecodeArgs a) {
   // through the loop has the same loads in flight and the memory waits stay
   // exact; the main loop has no early exit, the last one or two blocks run
   // after it.
+  // The zero-point table covers kChunk blocks; long splits refill it
+  // between chunks.
   if (nblocks > 0) {
     int i = 0;
-    for (; i + 3 <= nblocks; i += 3) {
-      load(min(i + 2, last), b2);
-      process(b0, i);
-      load(min(i + 3, last), b0);
-      process(b1, i + 1);
-      load(min(i + 4, last), b1);
-      process(b2, i + 2);
+    for (int c0 = 0; c0 < nblocks; c0 += kChunk) {
+      if (c0 > 0) {
+        h8_t zn[4];
+        load_z(c0 / BPG, zn);
+        fill_table(c0 / BPG, zn);
+      }
+      const int cend = min(nblocks, c0 + kChunk);
+      for (; i + 3 <= cend; i += 3) {
+        load(min(i + 2, last), b2);
+        process(b0, i);
+        load(min(i + 3, last), b0);
+        process(b1, i + 1);
+        load(min(i + 4, last), b1);
+        process(b2, i + 2);
+      }
     }
     if (i < nblocks) process(b0, i);
     if (i + 1 < nblocks) process(b1, i + 1);

@@ -130,6 +130,22 @@ def test_split_independence_and_determinism():
         assert row_rel_err(a[0], outs[128][0].astype(np.float64)).max() <= ATTN_TOL
 
 
+@pytest.mark.parametrize("gk,bk,bv", [(32, 1, 1), (64, 2, 1), (128, 1, 2)])
+def test_long_splits(gk, bk, bv):
+    # One split per head: every wave of the matrix kernel takes more than
+    # 48 blocks, so the per-wave zero-point table is refilled (and each fill
+    # covers more than 16 key groups); a 3-token fp16 tail rides along.
+    w = W(f"long_split_g{gk}_k{bk}v{bv}", 1, 32, 8, 6400 + 3 * gk + 3, bk, bv, gk=gk)
+    c = Case(w)
+    c.append_all()
+    kvq_set = __import__("paper_2607_16248_amd").kvq_set_split_tokens
+    kvq_set(c.cache.handle, (w.lens[0] // gk + 1) * gk)
+    out = c.decode()
+    err = row_rel_err(out[0], c.oracle_out(0)).max()
+    log(f"[parity] {w.name}: max row-relative error {err:.3e}")
+    assert err <= ATTN_TOL
+
+
 def test_empty_and_single_token_sequences():
     w = W("tiny", 3, 32, 8, (0, 1, 40), 1, 1)
     c = Case(w)
