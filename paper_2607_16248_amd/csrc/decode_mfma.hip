@@ -89,6 +89,11 @@ __device__ __forceinline__ h8_t unpack8(uint32_t x, int blk4, int plane) {
   return __builtin_bit_cast(h8_t, w);
 }
 
+// Keeps two fp32 results as such: an fma whose result is only converted to
+// fp16 would otherwise become v_fma_mixlo/mixhi_f16, which issue at half the
+// rate of v_fma_mix_f32 plus one v_cvt_pk_f16_f32 per pair.
+__device__ __forceinline__ void keep_f32(float& a, float& b) { asm("" : "+v"(a), "+v"(b)); }
+
 __device__ __forceinline__ f4_t mfma(h8_t a, h8_t b, f4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
@@ -409,10 +414,12 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const h2_t s2 = u2h(cur.sv[t]);
-      const float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
+      float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
+      keep_f32(f0, f1);
       const h2_t hi = (h2_t){(_Float16)f0, (_Float16)f1};  // nearest: the residuals carry both signs
-      const float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
-      const float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
+      float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
+      float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
+      keep_f32(g0, g1);
       bhi[t] = h2u(hi);
       blo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
       const h2_t z2 = u2h(cur.zv[t]);
