@@ -86,7 +86,7 @@ __device__ __forceinline__ void pack_value_blocks_matrix(const uint8_t* codes, i
       for (int e = 0; e < 8; ++e) {
         const int c = 16 * (4 * d + m4) + cl;
         const int r = e < 4 ? 4 * kg + e : 16 + 4 * kg + (e - 4);
-        v |= (uint32_t)((codes[(blk * 32 + r) * kHeadDim + c] >> p) & 1u) << pair_bit(m4, e);
+        v |= (uint32_t)((codes[(blk * 32 + r) * kHeadDim + c] >> p) & 1u) << value_elem_bit(m4, e);
       }
     reinterpret_cast<uint32_t*>(dst + (size_t)blk * 512 * bits)[w] = v;
   }

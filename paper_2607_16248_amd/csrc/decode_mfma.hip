@@ -25,15 +25,17 @@
 //     through 512 bytes of LDS per wave; output columns whose group differs
 //     from the channel's are discarded.
 //
-// Packed bits become operands with one shift per 4-element block and one
-// AND per element pair: a set bit at mantissa position w of a half is the
-// exact fp16 subnormal 2^(w - 24), and the shift puts every bit among the
-// top mantissa positions, where the matrix cores keep the products of such
-// subnormals to near fp32 precision (see unpack8).  Element pair i of a
-// block weighs 2^i: on the key side this weight depends only on the channel
-// and is folded into q~ once per decode; on the value side it is the token
-// pair and is folded into the weights p; the common 2^(B0 - 24) goes into
-// the fp32 scales.  The layouts that place the bits are in kvq_layout.h.
+// Packed key bits become operands with one shift per 4-element block and
+// one AND per element pair: a set bit at mantissa position w of a half is
+// the exact fp16 subnormal 2^(w - 24), and the shift puts every bit among
+// the top mantissa positions, where the matrix cores keep the products of
+// such subnormals to near fp32 precision (see unpack8).  Element pair i of a
+// block weighs 2^i, a weight that depends only on the channel and is folded
+// into q~ once per decode; the common 2^(B0 - 24) goes into the fp32 scale.
+// A value operand (8 tokens of one channel) is one byte of packed bits and
+// comes from a 256-entry LDS table of 8 halves, 0 or 2^plane each: an LDS
+// read instead of five vector instructions, with exact normal operands.
+// The layouts that place the bits are in kvq_layout.h.
 #include <hip/hip_runtime.h>
 
 #include "decode_common.h"
@@ -199,12 +201,21 @@ decode_mfma_kernel(DecodeArgs a) {
   __shared__ float qp_lds[kWaves][kHeadDim * kGQ];                          // fp16 tail split only
   __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * kGQ];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<kGQ> red;
+  // value operand of each byte of packed bits, per bit plane: half e = 2^plane * bit e
+  __shared__ __attribute__((aligned(16))) uint32_t vtab[BV][256 * 4];
 
   const Work wk = find_work(a);
   const DecodeSeq& S = a.seq[wk.si];
   const uint8_t* blk = a.arena + S.head0 + (uint64_t)wk.h * a.head_stride;
   // wave index as a scalar so that per-wave loop bounds stay in SGPRs
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+  for (int i = threadIdx.x; i < BV * 256 * 4; i += blockDim.x) {
+    const int p = i >> 10, byte = (i >> 2) & 255, k = i & 3;
+    const uint32_t one = p ? 0x4000u : 0x3C00u;  // 2^p as fp16
+    vtab[p][i & 1023] = (((byte >> (2 * k)) & 1) ? one : 0u) | (((byte >> (2 * k + 1)) & 1) ? one << 16 : 0u);
+  }
+  __syncthreads();
 
   if (wk.sp >= S.nq) {  // fp16 tail tokens: vector path
     float qs0[kGQ], qs1[kGQ];
@@ -319,12 +330,9 @@ decode_mfma_kernel(DecodeArgs a) {
   if (nblocks > 0) fill_table(0, zq);
 
   // Score layout: m = the softmax reference of head row (uniform over the
-  // row), mo0 / mo1 = m plus the pair weights ta, ta + 2 of the lane's two
-  // tokens (see the rescale below), l = the sum of the lane's own weights
-  // times 2^-ta.  Value layout:
-  // zacc[t] = the zero-point term of element pair t of the lane's group.
-  float m = -__builtin_inff(), mo0 = 0.f, mo1 = 0.f, l = 0.f;
-  float zacc[4] = {0.f, 0.f, 0.f, 0.f};
+  // row), l = the sum of the lane's own weights.  Value layout: zacc = the
+  // zero-point term of the lane's group over its tokens.
+  float m = -__builtin_inff(), l = 0.f, zacc = 0.f;
   f4_t acc[8];
 #pragma unroll
   for (int mb = 0; mb < 8; ++mb) acc[mb] = (f4_t){0.f, 0.f, 0.f, 0.f};
@@ -384,20 +392,14 @@ decode_mfma_kernel(DecodeArgs a) {
       const float alpha = __builtin_amdgcn_exp2f(m - mnew);  // 1 where the reference stays
       l *= alpha;
       m = mnew;
-      // the value operand's element pair of this lane's token of tile 0 is
-      // ta = (col >> 1) & 1 (tile 1: ta + 2); its weight 2^-ta goes into p
-      mo0 = m + (float)((__lane_id() >> 1) & 1);
-      mo1 = mo0 + 2.f;
       const float av = __shfl(alpha, 16 * hc);  // the same factor in the value layout
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) acc[mb] *= av;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) zacc[t] *= av;
+      zacc *= av;
     }
-    // p * 2^-t for the lane's two tokens (element pairs ta and ta + 2)
-    const float e0 = __builtin_amdgcn_exp2f(fmaf(raw0, cs, -mo0));
-    const float e1 = __builtin_amdgcn_exp2f(fmaf(raw1, cs, -mo1));
-    l += fmaf(e1, 4.f, e0);
+    const float e0 = __builtin_amdgcn_exp2f(fmaf(raw0, cs, -m));
+    const float e1 = __builtin_amdgcn_exp2f(fmaf(raw1, cs, -m));
+    l += e0 + e1;
     // to the value layout: lane (col, row) needs tokens 4*row + 0..3 and
     // 16 + 4*row + 0..3 of head hc
     wave_lds_sync();
@@ -416,21 +418,24 @@ decode_mfma_kernel(DecodeArgs a) {
       const h2_t s2 = u2h(cur.sv[t]);
       float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
       keep_f32(f0, f1);
-      const h2_t hi = (h2_t){(_Float16)f0, (_Float16)f1};  // nearest: the residuals carry both signs
+      uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});  // nearest: the residuals carry both signs
+      asm("" : "+v"(hw));  // the residuals read the packed halves
+      const h2_t hi = u2h(hw);
       float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
       float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
       keep_f32(g0, g1);
-      bhi[t] = h2u(hi);
+      bhi[t] = hw;
       blo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
       const h2_t z2 = u2h(cur.zv[t]);
-      zacc[t] = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc[t]));
+      zacc = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc));
     }
     const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
 #pragma unroll
       for (int p2 = 0; p2 < BV; ++p2) {
-        const h8_t av = unpack8<BV>(cur.vx[(mb >> 2) * BV + p2], mb & 3, p2);
+        const uint32_t byte = (cur.vx[(mb >> 2) * BV + p2] >> (8 * (mb & 3))) & 0xFFu;
+        const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[p2][byte * 4]);
         acc[mb] = mfma(av, BH, acc[mb]);
         acc[mb] = mfma(av, BL, acc[mb]);
       }
@@ -470,22 +475,20 @@ decode_mfma_kernel(DecodeArgs a) {
   // the loop's register budget free of epilogue-only values.
   const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int ecol = ln & 15, erow = ln >> 4, ehc = ecol >> 2, exc = ecol & 3;
-  // l: undo 2^-ta and sum the 16 lanes of the head's row; zacc: undo the
-  // pair weights and sum over the lane rows (the tokens of a group column)
-  l = ldexpf(l, (ecol >> 1) & 1);
+  // l: sum the 16 lanes of the head's row; zacc: sum over the lane rows
+  // (the tokens of a group column)
   l += dpp_mov<kQuadXor1>(0.f, l);
   l += dpp_mov<kQuadXor2>(0.f, l);
   l += dpp_mov<kHalfMirror>(0.f, l);
   l += dpp_mov<kMirror>(0.f, l);
-  float zs = fmaf(zacc[3], 8.f, fmaf(zacc[2], 4.f, fmaf(zacc[1], 2.f, zacc[0])));
+  float zs = zacc;
   zs += __shfl_xor(zs, 16);
   zs += __shfl_xor(zs, 32);
 #pragma unroll
   for (int mb = 0; mb < 8; ++mb) {
     if (exc == (16 * mb) / a.gv) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e)  // undo the code operand's 2^(B0 - 24)
-        red.acc[wv][ehc * kHeadDim + 16 * mb + 4 * erow + e] = fmaf(acc[mb][e], ldexpf(1.f, 24 - (7 - BV)), zs);
+      for (int e = 0; e < 4; ++e) red.acc[wv][ehc * kHeadDim + 16 * mb + 4 * erow + e] = acc[mb][e] + zs;
     }
   }
   if (ecol == 0) {

@@ -17,9 +17,10 @@
 //    value codes: blocks of 32 tokens, 512*b bytes each, in the lane order of
 //      the MFMA A-operand of O^T = V^T P: lane L = c%16 + 16*kg holds 2*b
 //      dwords; dword d*b + p covers channel blocks mb = 4d + m4 (m4 in 0..3),
-//      channel c = 16*mb + c%16, and the K-index element e' (0..7) at bit
-//      pair_bit(m4, e'), for block token r = tau(8*kg + e') where
+//      channel c = 16*mb + c%16, byte m4 holding the K-index elements e'
+//      (0..7, bit e' of the byte), for block token r = tau(8*kg + e') where
 //      tau(8*kg + e') = 4*kg + e' for e' < 4 and 16 + 4*kg + (e' - 4) otherwise.
+//      One byte is one A operand (8 halves), looked up in a 256-entry table.
 //    value meta: per 32-token block, scales s[g][pos(r)] then zeros
 //      z[g][pos(r)] (fp16, g < 128/Gv, r < 32): 128*(128/Gv) bytes, the same
 //      total as the canonical [t][g][(s, z)] order.  pos = tau^-1 puts the 8
@@ -53,13 +54,16 @@ KVQ_HD inline BitLoc key_bit(int c, int p, int b) {
   return {g * b + p, pair_bit(kb, e)};
 }
 
+// Bit of value-operand element e' (0..7) of channel block m4 (0..3) in its dword.
+KVQ_HD inline int value_elem_bit(int m4, int e) { return 8 * m4 + e; }
+
 // Value code bit of block token r (0..31), channel c, plane p.
 KVQ_HD inline BitLoc value_bit(int r, int c, int p, int b) {
   const int hi = r >> 4, r16 = r & 15;
   const int kg = r16 >> 2, e = (r16 & 3) + 4 * hi;
   const int mb = c >> 4, d = mb >> 2, m4 = mb & 3;
   const int lane = (c & 15) + 16 * kg;
-  return {lane * 2 * b + d * b + p, pair_bit(m4, e)};
+  return {lane * 2 * b + d * b + p, value_elem_bit(m4, e)};
 }
 
 // Position of block token r in a value meta row: tau^-1, so that
