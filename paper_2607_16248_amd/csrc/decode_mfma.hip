@@ -188,7 +188,13 @@ __device__ __forceinline__ float quad_bcast(float v) {
 // else two.
 template <int BK, int BV, int BPG>
 struct MatrixOcc {
-  static constexpr int value = BPG == 1 ? 3 : 2;
+  static constexpr int value = BPG == 1 ? (BK + BV == 2 ? 4 : 3) : 2;
+};
+// Blocks in flight per wave: at four waves per SIMD the registers hold two
+// block buffers (loads one block ahead), otherwise three.
+template <int BK, int BV, int BPG>
+struct MatrixStages {
+  static constexpr int value = MatrixOcc<BK, BV, BPG>::value >= 4 ? 2 : 3;
 };
 
 template <int BK, int BV, int BPG>
@@ -198,7 +204,6 @@ decode_mfma_kernel(DecodeArgs a) {
   // to kChunk key groups (16-byte aligned: rows are read with 16-byte loads)
   static_assert(kChunk * kGQ <= 3 * kQRow, "zero-point table rows");
   __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * kGQ + 3) * kQRow];
-  __shared__ float qp_lds[kWaves][kHeadDim * kGQ];                          // fp16 tail split only
   __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * kGQ];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<kGQ> red;
   // value operand of each byte of packed bits, per bit plane: half e = 2^plane * bit e
@@ -222,7 +227,8 @@ decode_mfma_kernel(DecodeArgs a) {
     load_q_scaled<kGQ>(a, S, wk.h, lane, qs0, qs1);
     State<kGQ> st;
     init_state<kGQ>(st);
-    tail_split<kGQ>(a, S, wk.h, blk, qs0, qs1, qp_lds[wv], p_lds[wv], st, lane, wv);
+    static_assert(kHeadDim * kGQ <= (3 * kGQ + 3) * kQRow, "tail query fits the Q' area");
+    tail_split<kGQ>(a, S, wk.h, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st, lane, wv);
     stage_state<kGQ>(st, red, lane, wv);
     __syncthreads();
     write_record<kGQ>(a, S, wk.h, wk.sp, red);
@@ -265,11 +271,12 @@ decode_mfma_kernel(DecodeArgs a) {
       zq[kb] = __builtin_bit_cast(h8_t, ld128(rs, j * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
   };
   // the first two blocks and the first zero-points load while the query is prepared
+  constexpr int kStages = MatrixStages<BK, BV, BPG>::value;
   BlockData<BK, BV> b0, b1, b2;
   h8_t zq[4];
   if (nblocks > 0) {
     load(0, b0);
-    load(min(1, last), b1);
+    if constexpr (kStages == 3) load(min(1, last), b1);
     load_z(0, zq);
   }
 
@@ -442,7 +449,8 @@ decode_mfma_kernel(DecodeArgs a) {
     }
   };
 
-  // Three buffers, loads two blocks ahead of the arithmetic.  The loads are
+  // Three buffers, loads two blocks ahead of the arithmetic (two buffers,
+  // one block ahead, at four waves per SIMD).  The loads are
   // unconditional (past the end they re-read the last block) so every path
   // through the loop has the same loads in flight and the memory waits stay
   // exact; the main loop has no early exit, the last one or two blocks run
@@ -458,17 +466,26 @@ decode_mfma_kernel(DecodeArgs a) {
         fill_table(c0 / BPG, zn);
       }
       const int cend = min(nblocks, c0 + kChunk);
-      for (; i + 3 <= cend; i += 3) {
-        load(min(i + 2, last), b2);
-        process(b0, i);
-        load(min(i + 3, last), b0);
-        process(b1, i + 1);
-        load(min(i + 4, last), b1);
-        process(b2, i + 2);
+      if constexpr (kStages == 3) {
+        for (; i + 3 <= cend; i += 3) {
+          load(min(i + 2, last), b2);
+          process(b0, i);
+          load(min(i + 3, last), b0);
+          process(b1, i + 1);
+          load(min(i + 4, last), b1);
+          process(b2, i + 2);
+        }
+      } else {
+        for (; i + 2 <= cend; i += 2) {
+          load(min(i + 1, last), b1);
+          process(b0, i);
+          load(min(i + 2, last), b0);
+          process(b1, i + 1);
+        }
       }
     }
     if (i < nblocks) process(b0, i);
-    if (i + 1 < nblocks) process(b1, i + 1);
+    if (kStages == 3 && i + 1 < nblocks) process(b1, i + 1);
   }
 
   // Lane coordinates again, from the lane id: recomputing them here keeps
