@@ -1,5 +1,5 @@
 // Matrix-core decode attention for caches with 1- or 2-bit keys and values
-// and four query heads per kv head (gfx950, v_mfma_f32_16x16x32_f16).
+// and 4, 5 or 8 query heads per kv head (gfx950, v_mfma_f32_16x16x32_f16).
 //
 // Same result as the vector kernel: softmax(q K^T / sqrt(d)) V over the
 // dequantized cache (Introduction: scaled dot-product attention), split-K
@@ -11,19 +11,20 @@
 //   scores:  S[row][t] = sum_c Q'[row][c] * code[t][c] + sum_c q~[row][c] * z[c]
 //     A = Q' = q~ (.) s split into fp16 hi + lo parts (two product terms,
 //         each exact: q~ and s are fp16, their product fits two halves),
-//         row = 4*head + x: x = 0, 2 carry hi, x = 1, 3 carry lo,
+//         row = 4*head + x for 4 heads (x = 0, 2 carry hi, x = 1, 3 lo) or
+//         2*head + x for up to 8 heads (x = 0 hi, 1 lo),
 //     B = key codes as exact fp16 0/1 (or 0/2 for the high bit plane).
-//     A lane of the result holds one token of one head (elements x), so
-//     every lane takes its own exponentials and a 16-lane row reduces the
-//     block maximum of its head.  The zero-point term uses A = q~ and B = z
+//     A lane of the result holds one token of one or two heads (elements
+//     x), so every lane takes its own exponentials and a 16-lane row reduces
+//     the block maximum of its heads.  The zero-point term uses A = q~ and B = z
 //     broadcast over tokens.  q~ = q * 2^-e with |q~| < 1 keeps every fp16
 //     operand finite; the scale 2^e * log2(e) / sqrt(d) is applied to the
 //     fp32 result.
 //   values:  O^T[c][col] = sum_t code[t][c] * P'[t][col] (+ z term on VALU)
 //     A = value codes (exact fp16), B = P' = p * s_v split hi / lo,
-//     column col = 4*head + value group; the weights p reach the B layout
-//     through 512 bytes of LDS per wave; output columns whose group differs
-//     from the channel's are discarded.
+//     column col = 4*head + value group (one MFMA pair per 4 heads); the
+//     weights p reach the B layout through LDS; output columns whose group
+//     differs from the channel's are discarded.
 //
 // Packed key bits become operands with one shift per 4-element block and
 // one AND per element pair: a set bit at mantissa position w of a half is
@@ -52,7 +53,6 @@ typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
 typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kGQ = 4;
 // Headroom of the softmax reference above the largest score seen (log2
 // units): weights of later tokens within it need no rescale.
 constexpr float kLazyMargin = 3.f;
@@ -111,8 +111,18 @@ __device__ __forceinline__ float max_across_rows(float v) {
   return fmaxf(__builtin_bit_cast(float, (uint32_t)s16[0]), __builtin_bit_cast(float, (uint32_t)s16[1]));
 }
 
-__device__ __forceinline__ float pick4(const float (&v)[kGQ], int i) {
-  return i == 0 ? v[0] : i == 1 ? v[1] : i == 2 ? v[2] : v[3];
+// v[i] as a chain of selects (keeps v in registers; an indexed read would
+// move the array to scratch memory).
+template <int K, int N>
+__device__ __forceinline__ float pick_from(const float (&v)[N], int i) {
+  if constexpr (K == N - 1)
+    return v[K];
+  else
+    return i == K ? v[K] : pick_from<K + 1, N>(v, i);
+}
+template <int N>
+__device__ __forceinline__ float pickn(const float (&v)[N], int i) {
+  return pick_from<0, N>(v, i);
 }
 
 // Buffer resource over one (sequence, kv head) block.  Every load is
@@ -183,29 +193,41 @@ __device__ __forceinline__ float quad_bcast(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), K * 0x55, 0xF, 0xF, false));
 }
 
-// Waves per SIMD the instantiation is compiled for: three where its
-// registers fit 168 without spilling (one 32-token block per key group),
-// else two.
-template <int BK, int BV, int BPG>
-struct MatrixOcc {
-  static constexpr int value = BPG == 1 ? (BK + BV == 2 ? 4 : 3) : 2;
+// Query heads per kv head the score rows carry: 4 (rows 4h + x, x = hi, lo,
+// hi, lo) or 8 (rows 2h + x, x = hi, lo); 5 heads use the 8-head layout with
+// three empty heads.
+template <int GQ>
+struct MatrixHeads {
+  static constexpr int value = GQ <= 4 ? 4 : 8;
 };
-// Blocks in flight per wave: at four waves per SIMD the registers hold two
-// block buffers (loads one block ahead), otherwise three.
-template <int BK, int BV, int BPG>
+// Waves per SIMD the instantiation is compiled for: four for 1-bit keys and
+// values with one 32-token block per key group, three for the other
+// four-head cases with one block per group, else two (registers).
+template <int BK, int BV, int BPG, int GQ>
+struct MatrixOcc {
+  static constexpr int value = GQ > 4 ? 2 : BPG == 1 ? (BK + BV == 2 ? 4 : 3) : 2;
+};
+// Blocks in flight per wave: at four waves per SIMD, and with the eight-head
+// accumulators, the registers hold two block buffers (loads one block
+// ahead), otherwise three.
+template <int BK, int BV, int BPG, int GQ>
 struct MatrixStages {
-  static constexpr int value = MatrixOcc<BK, BV, BPG>::value >= 4 ? 2 : 3;
+  static constexpr int value = (MatrixOcc<BK, BV, BPG, GQ>::value >= 4 || GQ > 4) ? 2 : 3;
 };
 
-template <int BK, int BV, int BPG>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MatrixOcc<BK, BV, BPG>::value))) void
+template <int BK, int BV, int BPG, int GQ>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MatrixOcc<BK, BV, BPG, GQ>::value))) void
 decode_mfma_kernel(DecodeArgs a) {
+  constexpr int NH = MatrixHeads<GQ>::value;  // heads in the score rows
+  constexpr int HPL = NH / 4;                 // heads per lane in the score layout
+  constexpr int NQ = NH / 4;                  // head quads in the value columns
+  constexpr int RS = 16 / NH;                 // score rows per head
+  constexpr int kDzRows = (kChunk * NH + kQRow - 1) / kQRow;
   // per wave: Q' hi rows, lo rows, q~ rows, then the zero-point terms of up
   // to kChunk key groups (16-byte aligned: rows are read with 16-byte loads)
-  static_assert(kChunk * kGQ <= 3 * kQRow, "zero-point table rows");
-  __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * kGQ + 3) * kQRow];
-  __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * kGQ];  // weights to the value layout; fp16 tail split
-  __shared__ Reduce<kGQ> red;
+  __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * NH + kDzRows) * kQRow];
+  __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * NH];  // weights to the value layout; fp16 tail split
+  __shared__ Reduce<GQ> red;
   // value operand of each byte of packed bits, per bit plane: half e = 2^plane * bit e
   __shared__ __attribute__((aligned(16))) uint32_t vtab[BV][256 * 4];
 
@@ -223,22 +245,25 @@ decode_mfma_kernel(DecodeArgs a) {
   __syncthreads();
 
   if (wk.sp >= S.nq) {  // fp16 tail tokens: vector path
-    float qs0[kGQ], qs1[kGQ];
-    load_q_scaled<kGQ>(a, S, wk.h, lane, qs0, qs1);
-    State<kGQ> st;
-    init_state<kGQ>(st);
-    static_assert(kHeadDim * kGQ <= (3 * kGQ + 3) * kQRow, "tail query fits the Q' area");
-    tail_split<kGQ>(a, S, wk.h, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st, lane, wv);
-    stage_state<kGQ>(st, red, lane, wv);
+    float qs0[GQ], qs1[GQ];
+    load_q_scaled<GQ>(a, S, wk.h, lane, qs0, qs1);
+    State<GQ> st;
+    init_state<GQ>(st);
+    static_assert(kHeadDim * QStride<GQ>::value <= (3 * NH + kDzRows) * kQRow, "tail query fits the Q' area");
+    static_assert(32 * GQ <= kPRow * NH, "tail weights fit the weight area");
+    tail_split<GQ>(a, S, wk.h, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st, lane, wv);
+    stage_state<GQ>(st, red, lane, wv);
     __syncthreads();
-    write_record<kGQ>(a, S, wk.h, wk.sp, red);
+    write_record<GQ>(a, S, wk.h, wk.sp, red);
     return;
   }
 
+  // Value layout: lane (col, row) = column (head 4q + hc, value group xc),
+  // tokens of K-group row.  Score A rows: row col = head hs, half part.
   const int col = lane & 15, row = lane >> 4;     // MFMA column, lane row
-  const int hc = col >> 2, xc = col & 3, part = col & 1;
+  const int hc = col >> 2, xc = col & 3, part = col & 1, hs = col / RS;
   const int ng = kHeadDim / a.gv, gsel = xc & (ng - 1);
-  const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * kGQ) * kHeadDim;
+  const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * GQ) * kHeadDim;
   const __amdgpu_buffer_rsrc_t rs = head_rsrc(blk, a.head_stride);
   LaneOffsets lo;
   lo.km = 4 * lane;
@@ -271,7 +296,7 @@ decode_mfma_kernel(DecodeArgs a) {
       zq[kb] = __builtin_bit_cast(h8_t, ld128(rs, j * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
   };
   // the first two blocks and the first zero-points load while the query is prepared
-  constexpr int kStages = MatrixStages<BK, BV, BPG>::value;
+  constexpr int kStages = MatrixStages<BK, BV, BPG, GQ>::value;
   BlockData<BK, BV> b0, b1, b2;
   h8_t zq[4];
   if (nblocks > 0) {
@@ -285,12 +310,21 @@ decode_mfma_kernel(DecodeArgs a) {
   // those channels in the unpacked key operand.
   const float wq = ldexpf(1.f, -(lane & 3));
   uint32_t* ql = q_lds[wv];
-  uint32_t* qq = ql + 2 * kGQ * kQRow;  // q~ of head g in row g
-  float* dzt = reinterpret_cast<float*>(ql + 3 * kGQ * kQRow);  // [group k mod (kChunk / BPG)][head]
-  uint32_t qt[kGQ];
-  float inv[kGQ], csc[kGQ];
+  uint32_t* qq = ql + 2 * NH * kQRow;  // q~ of head g in row g
+  float* dzt = reinterpret_cast<float*>(ql + 3 * NH * kQRow);  // [group k mod (kChunk / BPG)][head]
+  uint32_t qt[NH];
+  float inv[NH], csc[NH];
 #pragma unroll
-  for (int g = 0; g < kGQ; ++g) {
+  for (int g = GQ; g < NH; ++g) {  // empty heads: zero rows, scores 0
+    qt[g] = 0u;
+    inv[g] = 0.f;
+    csc[g] = 1.f;
+    qq[g * kQRow + lane] = 0u;
+    ql[g * kQRow + lane] = 0u;
+    ql[(NH + g) * kQRow + lane] = 0u;
+  }
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) {
     const uint32_t w = reinterpret_cast<const uint32_t*>(qrow + g * kHeadDim)[lane];
     const float q0 = h2f(w & 0xFFFF), q1 = h2f(w >> 16);
     const float mx = wave_max(fmaxf(fabsf(q0), fabsf(q1)));
@@ -304,21 +338,23 @@ decode_mfma_kernel(DecodeArgs a) {
     qt[g] = h2u(t);
     qq[g * kQRow + lane] = h2u((h2_t){(_Float16)(q0 * inv[g]), (_Float16)(q1 * inv[g])});
   }
-  // score layout: token col of the 16-token tile, head row
-  const float cs = pick4(csc, row);
+  // score layout: token col of the 16-token tile, heads HPL*row + hh
+  float cs[HPL];
+#pragma unroll
+  for (int hh = 0; hh < HPL; ++hh) cs[hh] = pickn<NH>(csc, HPL * row + hh);
 
-  // Zero-point terms sum_c z[c] q~[c] of 16 key groups and the 4 heads, in
-  // one MFMA chain (A = z of group col, B = q~ of head hc), scaled like the
-  // code products, into table rows s .. s + 15; lanes of column 4*head hold
-  // groups 4*row .. 4*row + 3.
+  // Zero-point terms sum_c z[c] q~[c] of 16 key groups and the NH heads, in
+  // one MFMA chain (A = z of group col, B = q~ of head col / RS), scaled like
+  // the code products, into table rows s .. s + 15; lanes of column RS*head
+  // hold groups 4*row .. 4*row + 3.
   auto dz_rows = [&](int s, const h8_t (&zq)[4]) {
     f4_t t = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
-      t = mfma(zq[kb], *reinterpret_cast<const h8_t*>(&qq[hc * kQRow + 16 * kb + 4 * row]), t);
-    if (xc == 0) {
+      t = mfma(zq[kb], *reinterpret_cast<const h8_t*>(&qq[hs * kQRow + 16 * kb + 4 * row]), t);
+    if (col % RS == 0) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) dzt[(s + 4 * row + e) * kGQ + hc] = t[e] * ldexpf(1.f, (7 - BK) - 24);
+      for (int e = 0; e < 4; ++e) dzt[(s + 4 * row + e) * NH + hs] = t[e] * ldexpf(1.f, (7 - BK) - 24);
     }
   };
   // The table for the wave's groups k0 .. k0 + kChunk / BPG - 1; zq holds
@@ -336,13 +372,23 @@ decode_mfma_kernel(DecodeArgs a) {
   };
   if (nblocks > 0) fill_table(0, zq);
 
-  // Score layout: m = the softmax reference of head row (uniform over the
-  // row), l = the sum of the lane's own weights.  Value layout: zacc = the
-  // zero-point term of the lane's group over its tokens.
-  float m = -__builtin_inff(), l = 0.f, zacc = 0.f;
-  f4_t acc[8];
+  // Score layout: m[hh] = the softmax reference of head HPL*row + hh
+  // (uniform over the row), l[hh] = the sum of the lane's own weights.
+  // Value layout: zacc[q] = the zero-point term of head 4q + hc, group xc
+  // over the lane's tokens; acc[q] the code term.
+  float m[HPL], l[HPL], zacc[NQ];
+  f4_t acc[NQ][8];
 #pragma unroll
-  for (int mb = 0; mb < 8; ++mb) acc[mb] = (f4_t){0.f, 0.f, 0.f, 0.f};
+  for (int hh = 0; hh < HPL; ++hh) {
+    m[hh] = -__builtin_inff();
+    l[hh] = 0.f;
+  }
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    zacc[q] = 0.f;
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) acc[q][mb] = (f4_t){0.f, 0.f, 0.f, 0.f};
+  }
 
   float* pl = p_lds[wv];
 
@@ -355,22 +401,26 @@ decode_mfma_kernel(DecodeArgs a) {
       // out through LDS
       wave_lds_sync();
 #pragma unroll
-      for (int g = 0; g < kGQ; ++g) {
+      for (int g = 0; g < GQ; ++g) {  // (the rows of empty heads stay zero)
         const h2_t q2 = u2h(qt[g]), s2 = u2h(cur.s);
         const h2_t hi = q2 * s2;
         const h2_t lo = __builtin_elementwise_fma(q2, s2, -hi);
         ql[g * kQRow + lane] = h2u(hi);
-        ql[(kGQ + g) * kQRow + lane] = h2u(lo);
+        ql[(NH + g) * kQRow + lane] = h2u(lo);
       }
       wave_lds_sync();
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
-        bp[kb] = *reinterpret_cast<const h8_t*>(&ql[(part * kGQ + hc) * kQRow + 16 * kb + 4 * row]);
-      // the group's zero-point term enters the hi row of the scores
-      dz = (f4_t){dzt[(k % kChunkGroups) * kGQ + row], 0.f, 0.f, 0.f};
+        bp[kb] = *reinterpret_cast<const h8_t*>(&ql[(part * NH + hs) * kQRow + 16 * kb + 4 * row]);
+      // the group's zero-point terms enter the hi rows of the scores
+      const float* dzr = dzt + (k % kChunkGroups) * NH + HPL * row;
+      if constexpr (HPL == 1)
+        dz = (f4_t){dzr[0], 0.f, 0.f, 0.f};
+      else
+        dz = (f4_t){dzr[0], 0.f, dzr[1], 0.f};
     }
 
-    // unscaled scores of token 16*mb + col for head row: hi + lo rows
+    // unscaled scores of token 16*mb + col for heads HPL*row + hh
     f4_t d[2];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
@@ -380,71 +430,107 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
         for (int p = 0; p < BK; ++p) d[mb] = mfma(bp[kb], unpack8<BK>(cur.kx[mb][p], kb, p), d[mb]);
     }
-    const float raw0 = d[0][0] + d[0][1], raw1 = d[1][0] + d[1][1];
+    float raw[HPL][2];
+#pragma unroll
+    for (int hh = 0; hh < HPL; ++hh)
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) raw[hh][mb] = d[mb][2 * hh] + d[mb][2 * hh + 1];  // hi + lo rows
 
-    // online softmax (base 2) for head row over these 32 tokens; cs > 0, so
-    // the maximum is taken before scaling.  The reference m moves only when a
+    // online softmax (base 2) per head over these 32 tokens; cs > 0, so the
+    // maximum is taken before scaling.  The reference m moves only when a
     // score exceeds it, and then to kLazyMargin above that score: every
     // weight stays <= 1, and the rescale of the accumulators (and its
     // exponential) is skipped while later maxima stay under the reference.
     const float ninf = -__builtin_inff();
-    float bm = fmaxf(raw0, raw1);
-    bm = fmaxf(bm, dpp_mov<kQuadXor1>(ninf, bm));
-    bm = fmaxf(bm, dpp_mov<kQuadXor2>(ninf, bm));
-    bm = fmaxf(bm, dpp_mov<kHalfMirror>(ninf, bm));
-    bm = fmaxf(bm, dpp_mov<kMirror>(ninf, bm));
-    bm *= cs;
-    if (__builtin_amdgcn_ballot_w64(bm > m)) {
-      const float mnew = bm > m ? bm + kLazyMargin : m;
-      const float alpha = __builtin_amdgcn_exp2f(m - mnew);  // 1 where the reference stays
-      l *= alpha;
-      m = mnew;
-      const float av = __shfl(alpha, 16 * hc);  // the same factor in the value layout
+    float bm[HPL];
+    bool up = false;
 #pragma unroll
-      for (int mb = 0; mb < 8; ++mb) acc[mb] *= av;
-      zacc *= av;
+    for (int hh = 0; hh < HPL; ++hh) {
+      float b = fmaxf(raw[hh][0], raw[hh][1]);
+      b = fmaxf(b, dpp_mov<kQuadXor1>(ninf, b));
+      b = fmaxf(b, dpp_mov<kQuadXor2>(ninf, b));
+      b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
+      b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
+      bm[hh] = b * cs[hh];
+      up |= bm[hh] > m[hh];
     }
-    const float e0 = __builtin_amdgcn_exp2f(fmaf(raw0, cs, -m));
-    const float e1 = __builtin_amdgcn_exp2f(fmaf(raw1, cs, -m));
-    l += e0 + e1;
+    if (__builtin_amdgcn_ballot_w64(up)) {
+      float alpha[HPL];
+#pragma unroll
+      for (int hh = 0; hh < HPL; ++hh) {
+        const float mnew = bm[hh] > m[hh] ? bm[hh] + kLazyMargin : m[hh];
+        alpha[hh] = __builtin_amdgcn_exp2f(m[hh] - mnew);  // 1 where the reference stays
+        l[hh] *= alpha[hh];
+        m[hh] = mnew;
+      }
+      // the same factors in the value layout: head H = 4q + hc sits in the
+      // score lanes of row H / HPL, as their element H % HPL
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int H = 4 * q + hc;
+        float av;
+        if constexpr (HPL == 1) {
+          av = __shfl(alpha[0], 16 * H);
+        } else {
+          const float a0 = __shfl(alpha[0], 16 * (H >> 1)), a1 = __shfl(alpha[1], 16 * (H >> 1));
+          av = (H & 1) ? a1 : a0;
+        }
+#pragma unroll
+        for (int mb = 0; mb < 8; ++mb) acc[q][mb] *= av;
+        zacc[q] *= av;
+      }
+    }
     // to the value layout: lane (col, row) needs tokens 4*row + 0..3 and
-    // 16 + 4*row + 0..3 of head hc
-    wave_lds_sync();
-    pl[row * kPRow + col] = e0;
-    pl[row * kPRow + 16 + col] = e1;
-    wave_lds_sync();
-    const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[hc * kPRow + 4 * row]);
-    const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[hc * kPRow + 16 + 4 * row]);
-    const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
-
-    // P' = p * s_v as fp16 hi + lo: the product and its residual are each
-    // one mixed-precision fma from the fp32 p and the fp16 scale
-    u4_t bhi, blo;
+    // 16 + 4*row + 0..3 of heads 4q + hc
+    float e[HPL][2];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const h2_t s2 = u2h(cur.sv[t]);
-      float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
-      keep_f32(f0, f1);
-      uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});  // nearest: the residuals carry both signs
-      asm("" : "+v"(hw));  // the residuals read the packed halves
-      const h2_t hi = u2h(hw);
-      float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
-      float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
-      keep_f32(g0, g1);
-      bhi[t] = hw;
-      blo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
-      const h2_t z2 = u2h(cur.zv[t]);
-      zacc = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc));
+    for (int hh = 0; hh < HPL; ++hh) {
+      e[hh][0] = __builtin_amdgcn_exp2f(fmaf(raw[hh][0], cs[hh], -m[hh]));
+      e[hh][1] = __builtin_amdgcn_exp2f(fmaf(raw[hh][1], cs[hh], -m[hh]));
+      l[hh] += e[hh][0] + e[hh][1];
     }
-    const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
+    wave_lds_sync();
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
+    for (int hh = 0; hh < HPL; ++hh) {
+      pl[(HPL * row + hh) * kPRow + col] = e[hh][0];
+      pl[(HPL * row + hh) * kPRow + 16 + col] = e[hh][1];
+    }
+    wave_lds_sync();
 #pragma unroll
-      for (int p2 = 0; p2 < BV; ++p2) {
-        const uint32_t byte = (cur.vx[(mb >> 2) * BV + p2] >> (8 * (mb & 3))) & 0xFFu;
-        const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[p2][byte * 4]);
-        acc[mb] = mfma(av, BH, acc[mb]);
-        acc[mb] = mfma(av, BL, acc[mb]);
+    for (int q = 0; q < NQ; ++q) {
+      const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[(4 * q + hc) * kPRow + 4 * row]);
+      const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[(4 * q + hc) * kPRow + 16 + 4 * row]);
+      const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
+
+      // P' = p * s_v as fp16 hi + lo: the product and its residual are each
+      // one mixed-precision fma from the fp32 p and the fp16 scale
+      u4_t bhi, blo;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const h2_t s2 = u2h(cur.sv[t]);
+        float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
+        keep_f32(f0, f1);
+        uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});  // nearest: the residuals carry both signs
+        asm("" : "+v"(hw));  // the residuals read the packed halves
+        const h2_t hi = u2h(hw);
+        float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
+        float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
+        keep_f32(g0, g1);
+        bhi[t] = hw;
+        blo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
+        const h2_t z2 = u2h(cur.zv[t]);
+        zacc[q] = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc[q]));
+      }
+      const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+#pragma unroll
+        for (int p2 = 0; p2 < BV; ++p2) {
+          const uint32_t byte = (cur.vx[(mb >> 2) * BV + p2] >> (8 * (mb & 3))) & 0xFFu;
+          const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[p2][byte * 4]);
+          acc[q][mb] = mfma(av, BH, acc[q][mb]);
+          acc[q][mb] = mfma(av, BL, acc[q][mb]);
+        }
       }
     }
   };
@@ -494,65 +580,99 @@ decode_mfma_kernel(DecodeArgs a) {
   const int ecol = ln & 15, erow = ln >> 4, ehc = ecol >> 2, exc = ecol & 3;
   // l: sum the 16 lanes of the head's row; zacc: sum over the lane rows
   // (the tokens of a group column)
-  l += dpp_mov<kQuadXor1>(0.f, l);
-  l += dpp_mov<kQuadXor2>(0.f, l);
-  l += dpp_mov<kHalfMirror>(0.f, l);
-  l += dpp_mov<kMirror>(0.f, l);
-  float zs = zacc;
-  zs += __shfl_xor(zs, 16);
-  zs += __shfl_xor(zs, 32);
 #pragma unroll
-  for (int mb = 0; mb < 8; ++mb) {
-    if (exc == (16 * mb) / a.gv) {
+  for (int hh = 0; hh < HPL; ++hh) {
+    l[hh] += dpp_mov<kQuadXor1>(0.f, l[hh]);
+    l[hh] += dpp_mov<kQuadXor2>(0.f, l[hh]);
+    l[hh] += dpp_mov<kHalfMirror>(0.f, l[hh]);
+    l[hh] += dpp_mov<kMirror>(0.f, l[hh]);
+  }
 #pragma unroll
-      for (int e = 0; e < 4; ++e) red.acc[wv][ehc * kHeadDim + 16 * mb + 4 * erow + e] = acc[mb][e] + zs;
+  for (int q = 0; q < NQ; ++q) {
+    float zs = zacc[q];
+    zs += __shfl_xor(zs, 16);
+    zs += __shfl_xor(zs, 32);
+    const int H = 4 * q + ehc;
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      if (H < GQ && exc == (16 * mb) / a.gv) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + e] = acc[q][mb][e] + zs;
+      }
     }
   }
   if (ecol == 0) {
-    red.m[wv][erow] = m;
-    red.l[wv][erow] = l;
+#pragma unroll
+    for (int hh = 0; hh < HPL; ++hh) {
+      const int H = HPL * erow + hh;
+      if (H < GQ) {
+        red.m[wv][H] = m[hh];
+        red.l[wv][H] = l[hh];
+      }
+    }
   }
   __syncthreads();
-  write_record<kGQ>(a, S, wk.h, wk.sp, red);
+  write_record<GQ>(a, S, wk.h, wk.sp, red);
 }
 
-template <int BK, int BV, int BPG>
+template <int BK, int BV, int BPG, int GQ>
 int launch_t(const DecodeArgs& a, void* stream) {
-  hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG>), dim3(a.total_wg), dim3(64 * kWaves), 0, (hipStream_t)stream,
-                     a);
+  hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG, GQ>), dim3(a.total_wg), dim3(64 * kWaves), 0,
+                     (hipStream_t)stream, a);
   return (int)hipGetLastError();
 }
 
-template <int BK, int BV>
-int launch_bpg(const DecodeArgs& a, void* stream) {
-  switch (a.gk / 32) {
-    case 1: return launch_t<BK, BV, 1>(a, stream);
-    case 2: return launch_t<BK, BV, 2>(a, stream);
-    case 4: return launch_t<BK, BV, 4>(a, stream);
+template <int BK, int BV, int BPG>
+int launch_gq(const DecodeArgs& a, int gq, void* stream) {
+  switch (gq) {
+    case 4: return launch_t<BK, BV, BPG, 4>(a, stream);
+    case 5: return launch_t<BK, BV, BPG, 5>(a, stream);
+    case 8: return launch_t<BK, BV, BPG, 8>(a, stream);
     default: return (int)hipErrorInvalidValue;
   }
 }
 
+template <int BK, int BV>
+int launch_bpg(const DecodeArgs& a, int gq, void* stream) {
+  switch (a.gk / 32) {
+    case 1: return launch_gq<BK, BV, 1>(a, gq, stream);
+    case 2: return launch_gq<BK, BV, 2>(a, gq, stream);
+    case 4: return launch_gq<BK, BV, 4>(a, gq, stream);
+    default: return (int)hipErrorInvalidValue;
+  }
+}
+
+template <int BK, int BV, int BPG>
+int occ_gq(int gq) {
+  return gq == 4 ? MatrixOcc<BK, BV, BPG, 4>::value : gq == 5 ? MatrixOcc<BK, BV, BPG, 5>::value
+                                                               : MatrixOcc<BK, BV, BPG, 8>::value;
+}
+
+template <int BK, int BV>
+int occ_bpg(int gk, int gq) {
+  return gk == 32 ? occ_gq<BK, BV, 1>(gq) : gk == 64 ? occ_gq<BK, BV, 2>(gq) : occ_gq<BK, BV, 4>(gq);
+}
+
 }  // namespace
 
-int matrix_decode_occupancy(int bk, int bv, int gk) {
-  const int bpg = gk / 32;
-  if (bk == 1 && bv == 1) return bpg == 1 ? MatrixOcc<1, 1, 1>::value : bpg == 2 ? MatrixOcc<1, 1, 2>::value : MatrixOcc<1, 1, 4>::value;
-  if (bk == 1 && bv == 2) return bpg == 1 ? MatrixOcc<1, 2, 1>::value : bpg == 2 ? MatrixOcc<1, 2, 2>::value : MatrixOcc<1, 2, 4>::value;
-  if (bk == 2 && bv == 1) return bpg == 1 ? MatrixOcc<2, 1, 1>::value : bpg == 2 ? MatrixOcc<2, 1, 2>::value : MatrixOcc<2, 1, 4>::value;
-  return bpg == 1 ? MatrixOcc<2, 2, 1>::value : bpg == 2 ? MatrixOcc<2, 2, 2>::value : MatrixOcc<2, 2, 4>::value;
+int matrix_decode_occupancy(int bk, int bv, int gk, int gq) {
+  if (bk == 1 && bv == 1) return occ_bpg<1, 1>(gk, gq);
+  if (bk == 1 && bv == 2) return occ_bpg<1, 2>(gk, gq);
+  if (bk == 2 && bv == 1) return occ_bpg<2, 1>(gk, gq);
+  return occ_bpg<2, 2>(gk, gq);
 }
 
 bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes) {
-  return gq == kGQ && (bk == 1 || bk == 2) && (bv == 1 || bv == 2) && gv >= 32 && head_bytes <= 0xFFFFFFFFull;
+  return (gq == 4 || gq == 5 || gq == 8) && (bk == 1 || bk == 2) && (bv == 1 || bv == 2) && gv >= 32 &&
+         head_bytes <= 0xFFFFFFFFull;
 }
 
-int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, void* stream) {
+int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stream) {
   if (a.total_wg <= 0) return 0;
-  if (bk == 1 && bv == 1) return launch_bpg<1, 1>(a, stream);
-  if (bk == 1 && bv == 2) return launch_bpg<1, 2>(a, stream);
-  if (bk == 2 && bv == 1) return launch_bpg<2, 1>(a, stream);
-  if (bk == 2 && bv == 2) return launch_bpg<2, 2>(a, stream);
+  if (bk == 1 && bv == 1) return launch_bpg<1, 1>(a, gq, stream);
+  if (bk == 1 && bv == 2) return launch_bpg<1, 2>(a, gq, stream);
+  if (bk == 2 && bv == 1) return launch_bpg<2, 1>(a, gq, stream);
+  if (bk == 2 && bv == 2) return launch_bpg<2, 2>(a, gq, stream);
   return (int)hipErrorInvalidValue;
 }
 

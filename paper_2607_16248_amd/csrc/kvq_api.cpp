@@ -216,7 +216,7 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   // the split plan fills one round of the lowest-occupancy kernel in use
   c->occupancy = 3;
   for (int i = 0; i < d->batch; ++i)
-    c->occupancy = std::min(c->occupancy, c->matrix[i] ? kvq::matrix_decode_occupancy(c->bk[i], c->bv[i], d->key_group)
+    c->occupancy = std::min(c->occupancy, c->matrix[i] ? kvq::matrix_decode_occupancy(c->bk[i], c->bv[i], d->key_group, d->num_q_heads / d->num_kv_heads)
                                                         : 2);
   *out = c;
   return ok();
@@ -388,7 +388,7 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.nseq = n;
     a.total_wg = wg;
     const int e = c->matrix[cls.second[0]]
-                      ? kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, stream)
+                      ? kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, d.num_q_heads / d.num_kv_heads, stream)
                       : kvq::launch_decode(a, cls.first.first, cls.first.second, d.num_q_heads / d.num_kv_heads, stream);
     if (e) return hip_fail(e, "decode launch");
   }

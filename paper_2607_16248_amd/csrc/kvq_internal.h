@@ -140,14 +140,14 @@ struct ExportArgs {
 // Launchers (defined next to their kernels).  Return a hipError_t as int.
 int launch_append(const AppendArgs& a, int bk, int bv, void* stream);
 int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
-int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, void* stream);
-// Matrix-core decode (and the matrix layout) for this bit class: 4 query
-// heads per kv head, 1- or 2-bit codes, value groups >= 32 channels, and a
-// (sequence, head) block that one buffer resource covers.
+int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
+// Matrix-core decode (and the matrix layout) for this bit class: 4, 5 or 8
+// query heads per kv head, 1- or 2-bit codes, value groups >= 32 channels,
+// and a (sequence, head) block that one buffer resource covers.
 bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes);
-// Waves per SIMD of the matrix-core kernel for this bit class (2 or 3); the
-// vector kernel runs two.
-int matrix_decode_occupancy(int bk, int bv, int gk);
+// Waves per SIMD of the matrix-core kernel for this bit class (2, 3 or 4);
+// the vector kernel runs two.
+int matrix_decode_occupancy(int bk, int bv, int gk, int gq);
 int launch_export(const ExportArgs& a, void* stream);
 int launch_merge(const MergeArgs& a, void* stream);
 int launch_dequant(const DequantArgs& a, void* stream);
