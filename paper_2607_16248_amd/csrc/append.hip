@@ -60,16 +60,24 @@ __device__ __forceinline__ void pack_rows(const uint8_t* codes, int rows, int bi
   }
 }
 
-// Matrix layout (kvq_layout.h), key rows: dword w of a row is plane p = w % b
-// of lane group g = w / b, gathering channels 32*kb + 8*g + e.
+// Matrix layout (kvq_layout.h), key rows.  1 and 2 bits: dword w of a row is
+// plane p = w % b of lane group g = w / b, gathering channels 32*kb + 8*g + e.
+// 4 and 8 bits: dword w holds 32/b whole codes, field f of channel
+// key_field_channel(w, f, b).
 __device__ __forceinline__ void pack_key_rows_matrix(const uint8_t* codes, int rows, int bits, uint8_t* dst) {
   const int dw_per_row = 4 * bits;
   for (int k = threadIdx.x; k < rows * dw_per_row; k += blockDim.x) {
-    const int i = k / dw_per_row, w = k % dw_per_row, g = w / bits, p = w % bits;
+    const int i = k / dw_per_row, w = k % dw_per_row;
     uint32_t v = 0;
-    for (int kb = 0; kb < 4; ++kb)
-      for (int e = 0; e < 8; ++e)
-        v |= (uint32_t)((codes[i * kHeadDim + 32 * kb + 8 * g + e] >> p) & 1u) << pair_bit(kb, e);
+    if (bits <= 2) {
+      const int g = w / bits, p = w % bits;
+      for (int kb = 0; kb < 4; ++kb)
+        for (int e = 0; e < 8; ++e)
+          v |= (uint32_t)((codes[i * kHeadDim + 32 * kb + 8 * g + e] >> p) & 1u) << pair_bit(kb, e);
+    } else {
+      for (int f = 0; f < 32 / bits; ++f)
+        v |= (uint32_t)codes[i * kHeadDim + key_field_channel(w, f, bits)] << (bits * f);
+    }
     reinterpret_cast<uint32_t*>(dst + (size_t)i * 16 * bits)[w] = v;
   }
 }
@@ -79,15 +87,23 @@ __device__ __forceinline__ void pack_value_blocks_matrix(const uint8_t* codes, i
   const int dw_per_block = 128 * bits;
   for (int k = threadIdx.x; k < (rows / 32) * dw_per_block; k += blockDim.x) {
     const int blk = k / dw_per_block, w = k % dw_per_block;
-    const int lane = w / (2 * bits), rem = w % (2 * bits), d = rem / bits, p = rem % bits;
-    const int cl = lane & 15, kg = lane >> 4;
     uint32_t v = 0;
-    for (int m4 = 0; m4 < 4; ++m4)
-      for (int e = 0; e < 8; ++e) {
-        const int c = 16 * (4 * d + m4) + cl;
-        const int r = e < 4 ? 4 * kg + e : 16 + 4 * kg + (e - 4);
-        v |= (uint32_t)((codes[(blk * 32 + r) * kHeadDim + c] >> p) & 1u) << value_elem_bit(m4, e);
+    if (bits <= 2) {
+      const int lane = w / (2 * bits), rem = w % (2 * bits), d = rem / bits, p = rem % bits;
+      const int cl = lane & 15, kg = lane >> 4;
+      for (int m4 = 0; m4 < 4; ++m4)
+        for (int e = 0; e < 8; ++e) {
+          const int c = 16 * (4 * d + m4) + cl;
+          const int r = value_token(kg, e);
+          v |= (uint32_t)((codes[(blk * 32 + r) * kHeadDim + c] >> p) & 1u) << value_elem_bit(m4, e);
+        }
+    } else {
+      for (int f = 0; f < 32 / bits; ++f) {
+        int r, c;
+        value_field_loc(w, f, bits, r, c);
+        v |= (uint32_t)codes[(blk * 32 + r) * kHeadDim + c] << (bits * f);
       }
+    }
     reinterpret_cast<uint32_t*>(dst + (size_t)blk * 512 * bits)[w] = v;
   }
 }

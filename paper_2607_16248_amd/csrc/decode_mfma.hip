@@ -1,5 +1,6 @@
-// Matrix-core decode attention for caches with 1- or 2-bit keys and values
-// and 4, 5 or 8 query heads per kv head (gfx950, v_mfma_f32_16x16x32_f16).
+// Matrix-core decode attention for caches with 1- or 2-bit keys and values,
+// or 4- or 8-bit keys and values of one width, and 4, 5 or 8 query heads per
+// kv head (gfx950, v_mfma_f32_16x16x32_f16).
 //
 // Same result as the vector kernel: softmax(q K^T / sqrt(d)) V over the
 // dequantized cache (Introduction: scaled dot-product attention), split-K
@@ -13,7 +14,8 @@
 //         each exact: q~ and s are fp16, their product fits two halves),
 //         row = 4*head + x for 4 heads (x = 0, 2 carry hi, x = 1, 3 lo) or
 //         2*head + x for up to 8 heads (x = 0 hi, 1 lo),
-//     B = key codes as exact fp16 0/1 (or 0/2 for the high bit plane).
+//     B = key codes as exact fp16 (bit planes at 1 and 2 bits, whole codes
+//         at 4 and 8 bits).
 //     A lane of the result holds one token of one or two heads (elements
 //     x), so every lane takes its own exponentials and a 16-lane row reduces
 //     the block maximum of its heads.  The zero-point term uses A = q~ and B = z
@@ -36,6 +38,10 @@
 // A value operand (8 tokens of one channel) is one byte of packed bits and
 // comes from a 256-entry LDS table of 8 halves, 0 or 2^plane each: an LDS
 // read instead of five vector instructions, with exact normal operands.
+// At 4 and 8 bits a dword holds whole codes, and one instruction per
+// element pair turns them into subnormal halves (see whole8); a token then
+// carries 160-288 bytes for the same arithmetic, and the matrix cores keep
+// the vector ALUs free for the conversions.
 // The layouts that place the bits are in kvq_layout.h.
 #include <hip/hip_runtime.h>
 
@@ -90,6 +96,49 @@ __device__ __forceinline__ h8_t unpack8(uint32_t x, int blk4, int plane) {
   for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (kB0 + plane + i));
   return __builtin_bit_cast(h8_t, w);
 }
+
+// One MFMA operand from whole 4- or 8-bit codes (elements e = 0..7 of the
+// operand, layout in kvq_layout.h): each half is code * 2^(U - 24), an exact
+// fp16 subnormal with the code at mantissa bits U .. U + B - 1 (U = 0 for
+// 8 bits, 4 for 4 bits), one instruction per element pair (a byte permute,
+// or a shift and an AND).
+template <int B>
+__device__ __forceinline__ h8_t whole8(const uint32_t* x) {
+  u4_t w;
+  if constexpr (B == 8) {
+    // dword h holds elements 4h .. 4h + 3 in its bytes; the selector puts
+    // bytes (2i, 2i + 1) into the low bytes of the two halves (0x0C = zero)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      w[2 * h] = __builtin_amdgcn_perm(0u, x[h], 0x0C010C00u);
+      w[2 * h + 1] = __builtin_amdgcn_perm(0u, x[h], 0x0C030C02u);
+    }
+  } else {
+    // element pair i at nibbles (i, i + 4): moved to bits (4, 20)
+    w[0] = (x[0] << 4) & 0x00F000F0u;
+    w[1] = x[0] & 0x00F000F0u;
+    w[2] = (x[0] >> 4) & 0x00F000F0u;
+    w[3] = (x[0] >> 8) & 0x00F000F0u;
+  }
+  return __builtin_bit_cast(h8_t, w);
+}
+
+// Weights p reach up to 2^S (S = PShift) instead of 1 so that p * s_v, a
+// B operand in fp16 hi + lo halves, keeps its lo half out of the subnormal
+// range: with 4- and 8-bit values s_v is small (range / 15 or / 255).  S is
+// the largest shift with p * s_v < 65504 for every valid scale (s_v <= 514
+// at 8 bits, 8736 at 4 bits; p <= 1 before the shift).
+template <int B>
+struct PShift {
+  static constexpr int value = B == 8 ? 6 : B == 4 ? 2 : 0;
+};
+
+// log2 of one code unit in an operand: bit planes at 1 and 2 bits (the
+// lowest plane sits at mantissa bit 7 - B), whole codes at 4 and 8 bits.
+template <int B>
+struct CodeUnit {
+  static constexpr int value = B <= 2 ? (7 - B) - 24 : B == 4 ? 4 - 24 : -24;
+};
 
 // Keeps two fp32 results as such: an fma whose result is only converted to
 // fp16 would otherwise become v_fma_mixlo/mixhi_f16, which issue at half the
@@ -168,10 +217,16 @@ __device__ __forceinline__ void load_block(__amdgpu_buffer_rsrc_t r, const LaneO
   for (int mb = 0; mb < 2; ++mb) {
     if constexpr (BK == 1) {
       o.kx[mb][0] = ld32(r, lo.kc + mb * 16 * 16 * BK, kc);
-    } else {
+    } else if constexpr (BK == 2) {
       const uint2 v = ld64(r, lo.kc + mb * 16 * 16 * BK, kc);
       o.kx[mb][0] = v.x;
       o.kx[mb][1] = v.y;
+    } else {
+#pragma unroll
+      for (int w = 0; w < BK / 4; ++w) {
+        const u4_t v = ld128(r, lo.kc + mb * 16 * 16 * BK + 16 * w, kc);
+        o.kx[mb][4 * w] = v[0]; o.kx[mb][4 * w + 1] = v[1]; o.kx[mb][4 * w + 2] = v[2]; o.kx[mb][4 * w + 3] = v[3];
+      }
     }
   }
   if constexpr (BV == 1) {
@@ -179,8 +234,11 @@ __device__ __forceinline__ void load_block(__amdgpu_buffer_rsrc_t r, const LaneO
     o.vx[0] = v.x;
     o.vx[1] = v.y;
   } else {
-    const u4_t v = ld128(r, lo.vc, vc);
-    o.vx[0] = v[0]; o.vx[1] = v[1]; o.vx[2] = v[2]; o.vx[3] = v[3];
+#pragma unroll
+    for (int w = 0; w < BV / 2; ++w) {
+      const u4_t v = ld128(r, lo.vc + 16 * w, vc);
+      o.vx[4 * w] = v[0]; o.vx[4 * w + 1] = v[1]; o.vx[4 * w + 2] = v[2]; o.vx[4 * w + 3] = v[3];
+    }
   }
   o.sv = ld128(r, lo.vs, vm);
   o.zv = ld128(r, lo.vz, vm);
@@ -201,18 +259,18 @@ struct MatrixHeads {
   static constexpr int value = GQ <= 4 ? 4 : 8;
 };
 // Waves per SIMD the instantiation is compiled for: four for 1-bit keys and
-// values with one 32-token block per key group, three for the other
-// four-head cases with one block per group, else two (registers).
+// values with one 32-token block per key group, three for the other 1- and
+// 2-bit four-head cases with one block per group, else two (registers).
 template <int BK, int BV, int BPG, int GQ>
 struct MatrixOcc {
-  static constexpr int value = GQ > 4 ? 2 : BPG == 1 ? (BK + BV == 2 ? 4 : 3) : 2;
+  static constexpr int value = (GQ > 4 || BK > 2 || BV > 2) ? 2 : BPG == 1 ? (BK + BV == 2 ? 4 : 3) : 2;
 };
-// Blocks in flight per wave: at four waves per SIMD, and with the eight-head
-// accumulators, the registers hold two block buffers (loads one block
-// ahead), otherwise three.
+// Blocks in flight per wave: at four waves per SIMD, with the eight-head
+// accumulators and with 8-bit blocks (41 registers each), the registers hold
+// two block buffers (loads one block ahead), otherwise three.
 template <int BK, int BV, int BPG, int GQ>
 struct MatrixStages {
-  static constexpr int value = (MatrixOcc<BK, BV, BPG, GQ>::value >= 4 || GQ > 4) ? 2 : 3;
+  static constexpr int value = (MatrixOcc<BK, BV, BPG, GQ>::value >= 4 || GQ > 4 || BK + BV >= 16) ? 2 : 3;
 };
 
 template <int BK, int BV, int BPG, int GQ>
@@ -223,13 +281,16 @@ decode_mfma_kernel(DecodeArgs a) {
   constexpr int NQ = NH / 4;                  // head quads in the value columns
   constexpr int RS = 16 / NH;                 // score rows per head
   constexpr int kDzRows = (kChunk * NH + kQRow - 1) / kQRow;
+  constexpr int kPShift = PShift<BV>::value;
   // per wave: Q' hi rows, lo rows, q~ rows, then the zero-point terms of up
   // to kChunk key groups (16-byte aligned: rows are read with 16-byte loads)
   __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * NH + kDzRows) * kQRow];
   __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * NH];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<GQ> red;
   // value operand of each byte of packed bits, per bit plane: half e = 2^plane * bit e
-  __shared__ __attribute__((aligned(16))) uint32_t vtab[BV][256 * 4];
+  // (1- and 2-bit values only)
+  constexpr int kTabPlanes = BV <= 2 ? BV : 1, kTabWords = BV <= 2 ? 256 * 4 : 4;
+  __shared__ __attribute__((aligned(16))) uint32_t vtab[kTabPlanes][kTabWords];
 
   const Work wk = find_work(a);
   const DecodeSeq& S = a.seq[wk.si];
@@ -237,12 +298,14 @@ decode_mfma_kernel(DecodeArgs a) {
   // wave index as a scalar so that per-wave loop bounds stay in SGPRs
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-  for (int i = threadIdx.x; i < BV * 256 * 4; i += blockDim.x) {
-    const int p = i >> 10, byte = (i >> 2) & 255, k = i & 3;
-    const uint32_t one = p ? 0x4000u : 0x3C00u;  // 2^p as fp16
-    vtab[p][i & 1023] = (((byte >> (2 * k)) & 1) ? one : 0u) | (((byte >> (2 * k + 1)) & 1) ? one << 16 : 0u);
+  if constexpr (BV <= 2) {
+    for (int i = threadIdx.x; i < BV * 256 * 4; i += blockDim.x) {
+      const int p = i >> 10, byte = (i >> 2) & 255, k = i & 3;
+      const uint32_t one = p ? 0x4000u : 0x3C00u;  // 2^p as fp16
+      vtab[p][i & 1023] = (((byte >> (2 * k)) & 1) ? one : 0u) | (((byte >> (2 * k + 1)) & 1) ? one << 16 : 0u);
+    }
+    __syncthreads();
   }
-  __syncthreads();
 
   if (wk.sp >= S.nq) {  // fp16 tail tokens: vector path
     float qs0[GQ], qs1[GQ];
@@ -308,7 +371,7 @@ decode_mfma_kernel(DecodeArgs a) {
   // q~ = q * 2^-e per head with max |q~| < 1.  For the code MFMA each lane's
   // channel pair (2*lane, 2*lane+1) also carries 2^-w, w = the bit weight of
   // those channels in the unpacked key operand.
-  const float wq = ldexpf(1.f, -(lane & 3));
+  const float wq = BK <= 2 ? ldexpf(1.f, -(lane & 3)) : 1.f;
   uint32_t* ql = q_lds[wv];
   uint32_t* qq = ql + 2 * NH * kQRow;  // q~ of head g in row g
   float* dzt = reinterpret_cast<float*>(ql + 3 * NH * kQRow);  // [group k mod (kChunk / BPG)][head]
@@ -331,7 +394,7 @@ decode_mfma_kernel(DecodeArgs a) {
     int e = 0;
     frexpf(mx, &e);
     inv[g] = ldexpf(1.f, -e);
-    csc[g] = ldexpf(a.qscale, e + 24 - (7 - BK));  // undoes 2^-e and the code operand's 2^(B0 - 24)
+    csc[g] = ldexpf(a.qscale, e - CodeUnit<BK>::value);  // undoes 2^-e and the code unit
     h2_t t;
     t.x = (_Float16)(q0 * inv[g] * wq);
     t.y = (_Float16)(q1 * inv[g] * wq);
@@ -354,7 +417,7 @@ decode_mfma_kernel(DecodeArgs a) {
       t = mfma(zq[kb], *reinterpret_cast<const h8_t*>(&qq[hs * kQRow + 16 * kb + 4 * row]), t);
     if (col % RS == 0) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) dzt[(s + 4 * row + e) * NH + hs] = t[e] * ldexpf(1.f, (7 - BK) - 24);
+      for (int e = 0; e < 4; ++e) dzt[(s + 4 * row + e) * NH + hs] = t[e] * ldexpf(1.f, CodeUnit<BK>::value);
     }
   };
   // The table for the wave's groups k0 .. k0 + kChunk / BPG - 1; zq holds
@@ -426,9 +489,14 @@ decode_mfma_kernel(DecodeArgs a) {
     for (int mb = 0; mb < 2; ++mb) {
       d[mb] = dz;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+      for (int kb = 0; kb < 4; ++kb) {
+        if constexpr (BK <= 2) {
 #pragma unroll
-        for (int p = 0; p < BK; ++p) d[mb] = mfma(bp[kb], unpack8<BK>(cur.kx[mb][p], kb, p), d[mb]);
+          for (int p = 0; p < BK; ++p) d[mb] = mfma(bp[kb], unpack8<BK>(cur.kx[mb][p], kb, p), d[mb]);
+        } else {
+          d[mb] = mfma(bp[kb], whole8<BK>(&cur.kx[mb][(BK / 4) * kb]), d[mb]);
+        }
+      }
     }
     float raw[HPL][2];
 #pragma unroll
@@ -441,6 +509,8 @@ decode_mfma_kernel(DecodeArgs a) {
     // score exceeds it, and then to kLazyMargin above that score: every
     // weight stays <= 1, and the rescale of the accumulators (and its
     // exponential) is skipped while later maxima stay under the reference.
+    // With a weight shift (PShift) m and every score are kept kPShift lower,
+    // so the weights reach 2^kPShift; m is the reference of the record.
     const float ninf = -__builtin_inff();
     float bm[HPL];
     bool up = false;
@@ -451,7 +521,7 @@ decode_mfma_kernel(DecodeArgs a) {
       b = fmaxf(b, dpp_mov<kQuadXor2>(ninf, b));
       b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
       b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
-      bm[hh] = b * cs[hh];
+      bm[hh] = kPShift ? fmaf(b, cs[hh], -(float)kPShift) : b * cs[hh];
       up |= bm[hh] > m[hh];
     }
     if (__builtin_amdgcn_ballot_w64(up)) {
@@ -524,10 +594,16 @@ decode_mfma_kernel(DecodeArgs a) {
       const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) {
+        if constexpr (BV <= 2) {
 #pragma unroll
-        for (int p2 = 0; p2 < BV; ++p2) {
-          const uint32_t byte = (cur.vx[(mb >> 2) * BV + p2] >> (8 * (mb & 3))) & 0xFFu;
-          const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[p2][byte * 4]);
+          for (int p2 = 0; p2 < BV; ++p2) {
+            const uint32_t byte = (cur.vx[(mb >> 2) * BV + p2] >> (8 * (mb & 3))) & 0xFFu;
+            const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[p2][byte * 4]);
+            acc[q][mb] = mfma(av, BH, acc[q][mb]);
+            acc[q][mb] = mfma(av, BL, acc[q][mb]);
+          }
+        } else {
+          const h8_t av = whole8<BV>(&cur.vx[(BV / 4) * mb]);
           acc[q][mb] = mfma(av, BH, acc[q][mb]);
           acc[q][mb] = mfma(av, BL, acc[q][mb]);
         }
@@ -587,6 +663,8 @@ decode_mfma_kernel(DecodeArgs a) {
     l[hh] += dpp_mov<kHalfMirror>(0.f, l[hh]);
     l[hh] += dpp_mov<kMirror>(0.f, l[hh]);
   }
+  // whole value codes enter the products as code * 2^CodeUnit
+  const float kAccScale = BV <= 2 ? 1.f : ldexpf(1.f, -CodeUnit<BV>::value);
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     float zs = zacc[q];
@@ -597,7 +675,8 @@ decode_mfma_kernel(DecodeArgs a) {
     for (int mb = 0; mb < 8; ++mb) {
       if (H < GQ && exc == (16 * mb) / a.gv) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + e] = acc[q][mb][e] + zs;
+        for (int e = 0; e < 4; ++e)
+          red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + e] = acc[q][mb][e] * kAccScale + zs;
       }
     }
   }
@@ -659,12 +738,14 @@ int matrix_decode_occupancy(int bk, int bv, int gk, int gq) {
   if (bk == 1 && bv == 1) return occ_bpg<1, 1>(gk, gq);
   if (bk == 1 && bv == 2) return occ_bpg<1, 2>(gk, gq);
   if (bk == 2 && bv == 1) return occ_bpg<2, 1>(gk, gq);
-  return occ_bpg<2, 2>(gk, gq);
+  if (bk == 2 && bv == 2) return occ_bpg<2, 2>(gk, gq);
+  if (bk == 4) return occ_bpg<4, 4>(gk, gq);
+  return occ_bpg<8, 8>(gk, gq);
 }
 
 bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes) {
-  return (gq == 4 || gq == 5 || gq == 8) && (bk == 1 || bk == 2) && (bv == 1 || bv == 2) && gv >= 32 &&
-         head_bytes <= 0xFFFFFFFFull;
+  const bool bits = ((bk == 1 || bk == 2) && (bv == 1 || bv == 2)) || (bk == bv && (bk == 4 || bk == 8));
+  return (gq == 4 || gq == 5 || gq == 8) && bits && gv >= 32 && head_bytes <= 0xFFFFFFFFull;
 }
 
 int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stream) {
@@ -673,6 +754,8 @@ int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stre
   if (bk == 1 && bv == 2) return launch_bpg<1, 2>(a, gq, stream);
   if (bk == 2 && bv == 1) return launch_bpg<2, 1>(a, gq, stream);
   if (bk == 2 && bv == 2) return launch_bpg<2, 2>(a, gq, stream);
+  if (bk == 4 && bv == 4) return launch_bpg<4, 4>(a, gq, stream);
+  if (bk == 8 && bv == 8) return launch_bpg<8, 8>(a, gq, stream);
   return (int)hipErrorInvalidValue;
 }
 

@@ -32,7 +32,7 @@ struct kvq_cache {
   std::vector<HeadLayout> lay;
   std::vector<int32_t> L, Lq;
   std::vector<uint8_t> matrix;  // 1: matrix layout and the matrix-core decode kernel
-  int occupancy = 2;             // resident decode workgroups per compute unit
+  std::vector<int> occupancy;    // resident decode workgroups per compute unit, per sequence's kernel
   int32_t split_tokens = 0;
 };
 
@@ -119,20 +119,24 @@ HeadLayout layout_of(const kvq_cache_desc* d, int bk, int bv) {
                           (int64_t)d->fp16_window + d->key_group);
 }
 
-int32_t split_tokens_for(const kvq_cache* c) {
+// Split length of one launch's sequences (one bit class): the launch fills
+// one round of the resident workgroups of its kernel.  Classes launch one
+// after another, so each gets the whole device.
+int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs) {
   const int gk = c->d.key_group;
   if (c->split_tokens > 0) return c->split_tokens;
   int64_t total = 0, lq_max = 0, tails = 0;
-  for (int i = 0; i < c->d.batch; ++i) {
+  int occ = 4;
+  for (int i : seqs) {
     total += (int64_t)c->Lq[i] * c->d.num_kv_heads;
     lq_max = std::max<int64_t>(lq_max, c->Lq[i]);
     if (c->L[i] > c->Lq[i]) tails += c->d.num_kv_heads;
+    occ = std::min(occ, c->occupancy[i]);
   }
   // The fp16-tail workgroups (one per sequence and kv head with tail tokens)
   // share the same round of resident workgroups: a workgroup that has to
   // wait for a free slot would add a whole split's time to the launch.
-  const int64_t target = std::max<int64_t>(target_workgroups(c->occupancy) - tails,
-                                           target_workgroups(c->occupancy) / 2);
+  const int64_t target = std::max<int64_t>(target_workgroups(occ) - tails, target_workgroups(occ) / 2);
   int64_t st = (total + target - 1) / target;
   st = std::max<int64_t>(st, (lq_max + kMaxSplits - 1) / kMaxSplits);
   st = (st + gk - 1) / gk * gk;
@@ -213,11 +217,11 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   for (int i = 0; i < d->batch; ++i)
     c->matrix.push_back(kvq::matrix_decode_supported(c->bk[i], c->bv[i], d->num_q_heads / d->num_kv_heads,
                                                      d->value_group, c->lay[i].stride) ? 1 : 0);
-  // the split plan fills one round of the lowest-occupancy kernel in use
-  c->occupancy = 3;
+  // the split plan of a launch fills one round of its kernel's workgroups
   for (int i = 0; i < d->batch; ++i)
-    c->occupancy = std::min(c->occupancy, c->matrix[i] ? kvq::matrix_decode_occupancy(c->bk[i], c->bv[i], d->key_group, d->num_q_heads / d->num_kv_heads)
-                                                        : 2);
+    c->occupancy.push_back(c->matrix[i] ? kvq::matrix_decode_occupancy(c->bk[i], c->bv[i], d->key_group,
+                                                                       d->num_q_heads / d->num_kv_heads)
+                                        : 2);
   *out = c;
   return ok();
 }
@@ -315,20 +319,25 @@ size_t kvq_workspace_bytes(const kvq_cache* c) {
 namespace {
 
 struct SplitPlan {
-  int32_t split_tokens = 0;
-  std::vector<int32_t> nq, ns, base;
+  std::vector<int32_t> st, nq, ns, base;  // per sequence: split length, packed splits, all splits, first record
   int64_t records = 0;
 };
 
 SplitPlan plan_splits(const kvq_cache* c) {
   SplitPlan p;
   const int B = c->d.batch;
-  p.split_tokens = split_tokens_for(c);
+  p.st.assign(B, 0);
+  std::map<std::pair<int, int>, std::vector<int>> classes;
+  for (int i = 0; i < B; ++i) classes[{c->bk[i], c->bv[i]}].push_back(i);
+  for (auto& cl : classes) {
+    const int32_t st = split_tokens_for(c, cl.second);
+    for (int i : cl.second) p.st[i] = st;
+  }
   p.nq.resize(B);
   p.ns.resize(B);
   p.base.resize(B);
   for (int i = 0; i < B; ++i) {
-    p.nq[i] = (c->Lq[i] + p.split_tokens - 1) / p.split_tokens;
+    p.nq[i] = (c->Lq[i] + p.st[i] - 1) / p.st[i];
     p.ns[i] = p.nq[i] + (c->L[i] > c->Lq[i] ? 1 : 0);
     p.base[i] = (int32_t)p.records;
     p.records += p.ns[i];
@@ -368,7 +377,7 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.kc = (uint32_t)lay.kc; a.km = (uint32_t)lay.km; a.vc = (uint32_t)lay.vc;
     a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
     a.hq = d.num_q_heads; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
-    a.split_tokens = p.split_tokens;
+    a.split_tokens = p.st[cls.second[0]];
     a.qscale = qscale;
     if (app) {
       a.K_new = static_cast<const uint16_t*>(app->K);

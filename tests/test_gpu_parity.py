@@ -47,6 +47,10 @@ SMALL = [
     W("window_bigger_than_L", 1, 32, 8, 100, 1, 1, R=300),
     W("k1v1_g128_L1100", 1, 32, 8, 1100, 1, 1, gk=128),
     W("mixed_asym_g64_gv64", 4, 32, 8, (700, 1300, 520, 64), (1, 2, 1, 2), (2, 1, 1, 2), gk=64, gv=64),
+    W("gq5_k4v4_R128_t3", 2, 40, 8, (1000, 517), 4, 4, R=128, dist="student_t3"),
+    W("gq5_k8v8_R128_t3", 2, 40, 8, (1200, 300), 8, 8, R=128, dist="student_t3"),
+    W("gq8_k4v4_g128", 1, 64, 8, 1500, 4, 4, gk=128),
+    W("k8v8_g64_gv64_L2000", 1, 32, 8, 2000, 8, 8, gk=64, gv=64),
 ]
 
 
@@ -130,7 +134,7 @@ def test_split_independence_and_determinism():
         assert row_rel_err(a[0], outs[128][0].astype(np.float64)).max() <= ATTN_TOL
 
 
-@pytest.mark.parametrize("gk,bk,bv", [(32, 1, 1), (64, 2, 1), (128, 1, 2)])
+@pytest.mark.parametrize("gk,bk,bv", [(32, 1, 1), (64, 2, 1), (128, 1, 2), (32, 8, 8), (64, 4, 4)])
 def test_long_splits(gk, bk, bv):
     # One split per head: every wave of the matrix kernel takes more than
     # 48 blocks, so the per-wave zero-point table is refilled (and each fill
