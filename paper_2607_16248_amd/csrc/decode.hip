@@ -151,23 +151,29 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   write_record<GQ>(a, S, wk.h, wk.sp, red);
 }
 
-// One workgroup per (sequence, query head): thread (part, c) folds the
-// records of splits part, part + 8, ... into a running (max, denominator,
-// channel c numerator), loading kMergeUnroll records at a time so that one
-// memory round trip covers them; the eight parts then meet in LDS.
+// One workgroup per (sequence, query head, 32-channel slice): thread
+// (part, c) folds the records of splits part, part + 8, ... into a running
+// (max, denominator, channel c numerator), loading kMergeUnroll records at a
+// time so that one memory round trip covers up to 136 splits; the eight
+// parts then meet in LDS.  Four slices per head spread a head's records over
+// four compute units.
 constexpr int kMergeParts = 8;
-constexpr int kMergeThreads = kMergeParts * kHeadDim;
-constexpr int kMergeUnroll = 16;
+constexpr int kMergeSlice = 32;
+constexpr int kMergeSlices = kHeadDim / kMergeSlice;
+constexpr int kMergeThreads = kMergeParts * kMergeSlice;
+constexpr int kMergeUnroll = 17;
 
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
-  __shared__ float sm[kMergeParts], sl[kMergeParts], sa[kMergeParts][kHeadDim];
-  const int si = blockIdx.x / a.hq, hq = blockIdx.x % a.hq;
+  __shared__ float sm[kMergeParts], sl[kMergeParts], sa[kMergeParts][kMergeSlice];
+  const int head = blockIdx.x / kMergeSlices, slice = blockIdx.x % kMergeSlices;
+  const int si = head / a.hq, hq = head % a.hq;
   const MergeSeq& S = a.seq[si];
-  const int tid = threadIdx.x, c = tid % kHeadDim, part = tid / kHeadDim;
+  const int tid = threadIdx.x, cs = tid % kMergeSlice, part = tid / kMergeSlice;
+  const int c = slice * kMergeSlice + cs;
   float* o = a.out + ((size_t)S.seq * a.hq + hq) * kHeadDim;
   const int n = S.nsplit;
   if (n == 0) {
-    if (tid < kHeadDim) o[tid] = 0.f;
+    if (tid < kMergeSlice) o[c] = 0.f;
     return;
   }
   const float* base = a.ws + ((size_t)S.ws_base * a.hq + hq) * kRecFloats;
@@ -183,7 +189,6 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
       lv[u] = r[1];
       av[u] = r[4 + c];
     }
-    // i < n is the same for every thread of a wave (two waves per part)
     float mx = M;
 #pragma unroll
     for (int u = 0; u < kMergeUnroll; ++u)
@@ -200,13 +205,13 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
       }
     M = mx;
   }
-  if (c == 0) {
+  if (cs == 0) {
     sm[part] = M;
     sl[part] = D;
   }
-  sa[part][c] = A;
+  sa[part][cs] = A;
   __syncthreads();
-  if (tid < kHeadDim) {
+  if (tid < kMergeSlice) {
     float mx = sm[0];
 #pragma unroll
     for (int p = 1; p < kMergeParts; ++p) mx = fmaxf(mx, sm[p]);
@@ -215,7 +220,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
     for (int p = 0; p < kMergeParts; ++p) {
       const float w = __builtin_amdgcn_exp2f(sm[p] - mx);  // a part without splits has sm = -inf: w = 0
       den = fmaf(w, sl[p], den);
-      num = fmaf(w, sa[p][c], num);
+      num = fmaf(w, sa[p][cs], num);
     }
     o[c] = num / den;
   }
@@ -266,7 +271,7 @@ int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream) {
 
 int launch_merge(const MergeArgs& a, void* stream) {
   if (a.nseq <= 0) return 0;
-  hipLaunchKernelGGL(merge_kernel, dim3(a.nseq * a.hq), dim3(kMergeThreads), 0, (hipStream_t)stream, a);
+  hipLaunchKernelGGL(merge_kernel, dim3(a.nseq * a.hq * kMergeSlices), dim3(kMergeThreads), 0, (hipStream_t)stream, a);
   return (int)hipGetLastError();
 }
 
