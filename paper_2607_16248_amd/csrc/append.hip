@@ -60,23 +60,17 @@ __device__ __forceinline__ void pack_rows(const uint8_t* codes, int rows, int bi
   }
 }
 
-// Matrix layout (kvq_layout.h), key rows.  1 and 2 bits: dword w of a row is
-// plane p = w % b of lane group g = w / b, gathering channels 32*kb + 8*g + e.
-// 4 and 8 bits: dword w holds 32/b whole codes, field f of channel
-// key_field_channel(w, f, b).
+// Matrix layout (kvq_layout.h), key rows: each bit of a row dword comes from
+// the channel and code bit key_bit_owner names.
 __device__ __forceinline__ void pack_key_rows_matrix(const uint8_t* codes, int rows, int bits, uint8_t* dst) {
   const int dw_per_row = 4 * bits;
   for (int k = threadIdx.x; k < rows * dw_per_row; k += blockDim.x) {
     const int i = k / dw_per_row, w = k % dw_per_row;
     uint32_t v = 0;
-    if (bits <= 2) {
-      const int g = w / bits, p = w % bits;
-      for (int kb = 0; kb < 4; ++kb)
-        for (int e = 0; e < 8; ++e)
-          v |= (uint32_t)((codes[i * kHeadDim + 32 * kb + 8 * g + e] >> p) & 1u) << pair_bit(kb, e);
-    } else {
-      for (int f = 0; f < 32 / bits; ++f)
-        v |= (uint32_t)codes[i * kHeadDim + key_field_channel(w, f, bits)] << (bits * f);
+    for (int q = 0; q < 32; ++q) {
+      int c, p;
+      key_bit_owner(w, q, bits, c, p);
+      v |= (uint32_t)((codes[i * kHeadDim + c] >> p) & 1u) << q;
     }
     reinterpret_cast<uint32_t*>(dst + (size_t)i * 16 * bits)[w] = v;
   }
@@ -88,21 +82,10 @@ __device__ __forceinline__ void pack_value_blocks_matrix(const uint8_t* codes, i
   for (int k = threadIdx.x; k < (rows / 32) * dw_per_block; k += blockDim.x) {
     const int blk = k / dw_per_block, w = k % dw_per_block;
     uint32_t v = 0;
-    if (bits <= 2) {
-      const int lane = w / (2 * bits), rem = w % (2 * bits), d = rem / bits, p = rem % bits;
-      const int cl = lane & 15, kg = lane >> 4;
-      for (int m4 = 0; m4 < 4; ++m4)
-        for (int e = 0; e < 8; ++e) {
-          const int c = 16 * (4 * d + m4) + cl;
-          const int r = value_token(kg, e);
-          v |= (uint32_t)((codes[(blk * 32 + r) * kHeadDim + c] >> p) & 1u) << value_elem_bit(m4, e);
-        }
-    } else {
-      for (int f = 0; f < 32 / bits; ++f) {
-        int r, c;
-        value_field_loc(w, f, bits, r, c);
-        v |= (uint32_t)codes[(blk * 32 + r) * kHeadDim + c] << (bits * f);
-      }
+    for (int q = 0; q < 32; ++q) {
+      int r, c, p;
+      value_bit_owner(w, q, bits, r, c, p);
+      v |= (uint32_t)((codes[(blk * 32 + r) * kHeadDim + c] >> p) & 1u) << q;
     }
     reinterpret_cast<uint32_t*>(dst + (size_t)blk * 512 * bits)[w] = v;
   }

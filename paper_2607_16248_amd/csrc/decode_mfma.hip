@@ -14,8 +14,7 @@
 //         each exact: q~ and s are fp16, their product fits two halves),
 //         row = 4*head + x for 4 heads (x = 0, 2 carry hi, x = 1, 3 lo) or
 //         2*head + x for up to 8 heads (x = 0 hi, 1 lo),
-//     B = key codes as exact fp16 (bit planes at 1 and 2 bits, whole codes
-//         at 4 and 8 bits).
+//     B = key codes as exact fp16.
 //     A lane of the result holds one token of one or two heads (elements
 //     x), so every lane takes its own exponentials and a 16-lane row reduces
 //     the block maximum of its heads.  The zero-point term uses A = q~ and B = z
@@ -28,16 +27,17 @@
 //     weights p reach the B layout through LDS; output columns whose group
 //     differs from the channel's are discarded.
 //
-// Packed key bits become operands with one shift per 4-element block and
-// one AND per element pair: a set bit at mantissa position w of a half is
-// the exact fp16 subnormal 2^(w - 24), and the shift puts every bit among
-// the top mantissa positions, where the matrix cores keep the products of
-// such subnormals to near fp32 precision (see unpack8).  Element pair i of a
-// block weighs 2^i, a weight that depends only on the channel and is folded
-// into q~ once per decode; the common 2^(B0 - 24) goes into the fp32 scale.
-// A value operand (8 tokens of one channel) is one byte of packed bits and
-// comes from a 256-entry LDS table of 8 halves, 0 or 2^plane each: an LDS
-// read instead of five vector instructions, with exact normal operands.
+// Packed key codes become operands with a shift or two and one AND per
+// element pair: a set bit at mantissa position w of a half is the exact fp16
+// subnormal 2^(w - 24), and the shifts put every code among the top mantissa
+// positions, where the matrix cores keep the products of such subnormals to
+// near fp32 precision (see unpack_bits).  An element pair's weight (2^i at
+// one bit, 1 or 4 at two bits) depends only on the channel and is folded
+// into q~ once per decode; the common code unit goes into the fp32 scale.
+// A value operand (8 tokens of one channel) comes from 256-entry LDS tables
+// indexed by bytes of packed codes: one byte at one bit (8 halves, 0 or 1),
+// two bytes at two bits (4 halves each, 0..3), exact normal numbers, one LDS
+// read per byte instead of several vector instructions.
 // At 4 and 8 bits a dword holds whole codes, and one instruction per
 // element pair turns them into subnormal halves (see whole8); a token then
 // carries 160-288 bytes for the same arithmetic, and the matrix cores keep
@@ -76,24 +76,35 @@ constexpr int kChunk = 48;
 __device__ __forceinline__ h2_t u2h(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
 __device__ __forceinline__ uint32_t h2u(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
 
-// One MFMA operand (8 halves) from the bits of 4-element block blk4 in x
-// (bit plane `plane` of a B-bit code): element pair i sits at bits
-// (s, s + 16), s = pair_bit(blk4, 2i) = 4*blk4 + i.  One shift moves the
-// block to mantissa positions B0 + plane + i with B0 = 7 - B, and one AND per
-// pair leaves each half equal to bit * 2^(B0 + plane + i - 24), an exact fp16
-// subnormal whose set bit is among the top mantissa bits 5..9.  (The matrix
+// One MFMA operand (8 halves) from the 1-bit codes of 4-element block blk4
+// in x: element pair i sits at bits (s, s + 16), s = pair_bit(blk4, 2i) =
+// 4*blk4 + i.  One shift moves the block to mantissa positions 6 + i, and one
+// AND per pair leaves each half equal to bit * 2^(6 + i - 24), an exact fp16
+// subnormal whose set bit is among the top mantissa bits 6..9.  (The matrix
 // cores add the products of subnormal fp16 inputs to about 2^-(13 + p)
-// relative precision for a set bit at mantissa position p; at 5..9 that is
-// 2^-18 or better.)  The other operand or the output carries 2^-i and
-// 2^(24 - B0); 2^plane is the bit's significance in the code.
-template <int B>
-__device__ __forceinline__ h8_t unpack8(uint32_t x, int blk4, int plane) {
-  constexpr int kB0 = 7 - B;
-  const int sh = 4 * blk4 - kB0 - plane;
+// relative precision for a set bit at mantissa position p; at 6..9 that is
+// 2^-19 or better.)  The other operand carries 2^-i.
+__device__ __forceinline__ h8_t unpack_bits(uint32_t x, int blk4) {
+  const int sh = 4 * blk4 - 6;
   const uint32_t src = sh > 0 ? x >> sh : x << -sh;
   u4_t w;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (kB0 + plane + i));
+  for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (6 + i));
+  return __builtin_bit_cast(h8_t, w);
+}
+
+// One MFMA operand from 2-bit codes: operand k (0, 1) of dword x holds
+// element pair i at bits 8k + 2i and 8k + 2i + 16.  Two shifts put pairs 0
+// and 1 (then 2 and 3) at mantissa bits 6-7 and 8-9, and one AND per pair
+// keeps them: halves code * 2^(6 - 24) for pairs 0, 2 and code * 2^(8 - 24)
+// for pairs 1, 3 (the other operand carries 1/4 for those).
+__device__ __forceinline__ h8_t unpack_pairs2(uint32_t x, int k) {
+  const uint32_t y1 = k ? x >> 2 : x << 6, y2 = k ? x >> 6 : x << 2;
+  u4_t w;
+  w[0] = y1 & 0x00C000C0u;
+  w[1] = y1 & 0x03000300u;
+  w[2] = y2 & 0x00C000C0u;
+  w[3] = y2 & 0x03000300u;
   return __builtin_bit_cast(h8_t, w);
 }
 
@@ -133,11 +144,12 @@ struct PShift {
   static constexpr int value = B == 8 ? 6 : B == 4 ? 2 : 0;
 };
 
-// log2 of one code unit in an operand: bit planes at 1 and 2 bits (the
-// lowest plane sits at mantissa bit 7 - B), whole codes at 4 and 8 bits.
+// log2 of one code unit in a key operand (the lowest element pair sits at
+// mantissa bit 6 at 1 and 2 bits, whole codes at bits 4.. and 0..), and in a
+// value operand (1 and 2 bits come from tables of exact normal halves).
 template <int B>
 struct CodeUnit {
-  static constexpr int value = B <= 2 ? (7 - B) - 24 : B == 4 ? 4 - 24 : -24;
+  static constexpr int value = B <= 2 ? 6 - 24 : B == 4 ? 4 - 24 : -24;
 };
 
 // Keeps two fp32 results as such: an fma whose result is only converted to
@@ -287,10 +299,10 @@ decode_mfma_kernel(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * NH + kDzRows) * kQRow];
   __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * NH];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<GQ> red;
-  // value operand of each byte of packed bits, per bit plane: half e = 2^plane * bit e
-  // (1- and 2-bit values only)
-  constexpr int kTabPlanes = BV <= 2 ? BV : 1, kTabWords = BV <= 2 ? 256 * 4 : 4;
-  __shared__ __attribute__((aligned(16))) uint32_t vtab[kTabPlanes][kTabWords];
+  // value operand halves of each byte of packed codes: 8 halves (bit e of
+  // the byte) at 1 bit, 4 halves (the 2-bit fields) at 2 bits
+  constexpr int kTabWords = BV == 1 ? 256 * 4 : BV == 2 ? 256 * 2 : 4;
+  __shared__ __attribute__((aligned(16))) uint32_t vtab[kTabWords];
 
   const Work wk = find_work(a);
   const DecodeSeq& S = a.seq[wk.si];
@@ -298,11 +310,17 @@ decode_mfma_kernel(DecodeArgs a) {
   // wave index as a scalar so that per-wave loop bounds stay in SGPRs
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 
-  if constexpr (BV <= 2) {
-    for (int i = threadIdx.x; i < BV * 256 * 4; i += blockDim.x) {
-      const int p = i >> 10, byte = (i >> 2) & 255, k = i & 3;
-      const uint32_t one = p ? 0x4000u : 0x3C00u;  // 2^p as fp16
-      vtab[p][i & 1023] = (((byte >> (2 * k)) & 1) ? one : 0u) | (((byte >> (2 * k + 1)) & 1) ? one << 16 : 0u);
+  if constexpr (BV == 1) {
+    for (int i = threadIdx.x; i < 256 * 4; i += blockDim.x) {
+      const int byte = i >> 2, k = i & 3;
+      vtab[i] = (((byte >> (2 * k)) & 1) ? 0x3C00u : 0u) | (((byte >> (2 * k + 1)) & 1) ? 0x3C000000u : 0u);
+    }
+    __syncthreads();
+  } else if constexpr (BV == 2) {
+    const uint32_t half_of[4] = {0x0000u, 0x3C00u, 0x4000u, 0x4200u};  // 0, 1, 2, 3 as fp16
+    for (int i = threadIdx.x; i < 256 * 2; i += blockDim.x) {
+      const int byte = i >> 1, k = i & 1;
+      vtab[i] = half_of[(byte >> (4 * k)) & 3] | (half_of[(byte >> (4 * k + 2)) & 3] << 16);
     }
     __syncthreads();
   }
@@ -371,7 +389,7 @@ decode_mfma_kernel(DecodeArgs a) {
   // q~ = q * 2^-e per head with max |q~| < 1.  For the code MFMA each lane's
   // channel pair (2*lane, 2*lane+1) also carries 2^-w, w = the bit weight of
   // those channels in the unpacked key operand.
-  const float wq = BK <= 2 ? ldexpf(1.f, -(lane & 3)) : 1.f;
+  const float wq = BK == 1 ? ldexpf(1.f, -(lane & 3)) : BK == 2 ? ((lane & 1) ? 0.25f : 1.f) : 1.f;
   uint32_t* ql = q_lds[wv];
   uint32_t* qq = ql + 2 * NH * kQRow;  // q~ of head g in row g
   float* dzt = reinterpret_cast<float*>(ql + 3 * NH * kQRow);  // [group k mod (kChunk / BPG)][head]
@@ -490,9 +508,10 @@ decode_mfma_kernel(DecodeArgs a) {
       d[mb] = dz;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        if constexpr (BK <= 2) {
-#pragma unroll
-          for (int p = 0; p < BK; ++p) d[mb] = mfma(bp[kb], unpack8<BK>(cur.kx[mb][p], kb, p), d[mb]);
+        if constexpr (BK == 1) {
+          d[mb] = mfma(bp[kb], unpack_bits(cur.kx[mb][0], kb), d[mb]);
+        } else if constexpr (BK == 2) {
+          d[mb] = mfma(bp[kb], unpack_pairs2(cur.kx[mb][kb >> 1], kb & 1), d[mb]);
         } else {
           d[mb] = mfma(bp[kb], whole8<BK>(&cur.kx[mb][(BK / 4) * kb]), d[mb]);
         }
@@ -594,14 +613,18 @@ decode_mfma_kernel(DecodeArgs a) {
       const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) {
-        if constexpr (BV <= 2) {
-#pragma unroll
-          for (int p2 = 0; p2 < BV; ++p2) {
-            const uint32_t byte = (cur.vx[(mb >> 2) * BV + p2] >> (8 * (mb & 3))) & 0xFFu;
-            const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[p2][byte * 4]);
-            acc[q][mb] = mfma(av, BH, acc[q][mb]);
-            acc[q][mb] = mfma(av, BL, acc[q][mb]);
-          }
+        if constexpr (BV == 1) {
+          const uint32_t byte = (cur.vx[mb >> 2] >> (8 * (mb & 3))) & 0xFFu;
+          const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[byte * 4]);
+          acc[q][mb] = mfma(av, BH, acc[q][mb]);
+          acc[q][mb] = mfma(av, BL, acc[q][mb]);
+        } else if constexpr (BV == 2) {
+          const uint32_t x = cur.vx[mb >> 1] >> (16 * (mb & 1));
+          const uint2 t0 = *reinterpret_cast<const uint2*>(&vtab[(x & 0xFFu) * 2]);
+          const uint2 t1 = *reinterpret_cast<const uint2*>(&vtab[((x >> 8) & 0xFFu) * 2]);
+          const h8_t av = __builtin_bit_cast(h8_t, (u4_t){t0.x, t0.y, t1.x, t1.y});
+          acc[q][mb] = mfma(av, BH, acc[q][mb]);
+          acc[q][mb] = mfma(av, BL, acc[q][mb]);
         } else {
           const h8_t av = whole8<BV>(&cur.vx[(BV / 4) * mb]);
           acc[q][mb] = mfma(av, BH, acc[q][mb]);

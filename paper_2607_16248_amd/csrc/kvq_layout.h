@@ -7,37 +7,38 @@
 //             This is also the export image's order.
 //
 //  matrix     (caches read by the matrix-core decode kernel)
-//    key rows: still 16*b bytes per token, but permuted so that the 32
-//      channels one lane of a 16x16x32 MFMA A-operand needs sit in one dword
-//      per bit plane: channel c = 32*kb + 8*g + e (kb, g in 0..3, e in 0..7)
-//      lives in dword b*g + p (bit plane p of its code) at bit
-//      pair_bit(kb, e) = 16*(e&1) + 8*(kb>>1) + 4*(kb&1) + (e>>1).
-//      Bits (pair_bit, pair_bit + 16) then hold a consecutive element pair,
-//      which one AND turns into two fp16 values (exact subnormal powers of 2).
+//    The codes one lane of a 16x16x32 MFMA operand needs (8 elements) sit
+//    together in the lane's dwords, placed so that a few shifts and ANDs, a
+//    byte permute or a table lookup turn them into the operand's halves.
+//    key rows: 16*b bytes per token; lane group g (0..3) of the operand owns
+//      row dwords [b*g, b*g + b) and channels c = 32*kb + 8*g + e (kb: the
+//      operand's 32-channel block, e: its element 0..7).  Per width:
+//      b = 1: dword g, bit pair_bit(kb, e) = 16*(e&1) + 8*(kb>>1) + 4*(kb&1)
+//             + (e>>1): bits (s, s + 16) hold a consecutive element pair, one
+//             AND after a shift per block makes two fp16 values;
+//      b = 2: dword 2*g + (kb>>1), code bits at 8*(kb&1) + 2*(e>>1) + 16*(e&1):
+//             two shifts and four ANDs place element pairs 0, 2 at mantissa
+//             bits 6-7 and pairs 1, 3 at bits 8-9;
+//      b = 4: dword 4*g + kb, nibble (e>>1) + 4*(e&1) (element pair i at
+//             nibbles i, i + 4);
+//      b = 8: dword 8*g + 2*kb + (e>>2), byte e&3.
 //    value codes: blocks of 32 tokens, 512*b bytes each, in the lane order of
 //      the MFMA A-operand of O^T = V^T P: lane L = c%16 + 16*kg holds 2*b
-//      dwords; dword d*b + p covers channel blocks mb = 4d + m4 (m4 in 0..3),
-//      channel c = 16*mb + c%16, byte m4 holding the K-index elements e'
-//      (0..7, bit e' of the byte), for block token r = tau(8*kg + e') where
+//      dwords; operand mb (channels 16*mb .. 16*mb + 15, channel c =
+//      16*mb + c%16) has elements e' (0..7) for block tokens r = tau(8*kg + e'),
 //      tau(8*kg + e') = 4*kg + e' for e' < 4 and 16 + 4*kg + (e' - 4) otherwise.
-//      One byte is one A operand (8 halves), looked up in a 256-entry table.
+//      b = 1: dword mb >> 2, bit 8*(mb&3) + e': one byte per operand, looked
+//             up in a 256-entry table of 8 halves;
+//      b = 2: dword mb >> 1, bits 16*(mb&1) + 2*e': two bytes per operand,
+//             each looked up in a 256-entry table of 4 halves;
+//      b = 4: dword mb, nibble (e'>>1) + 4*(e'&1);
+//      b = 8: dword 2*mb + (e'>>2), byte e'&3.
 //    value meta: per 32-token block, scales s[g][pos(r)] then zeros
 //      z[g][pos(r)] (fp16, g < 128/Gv, r < 32): 128*(128/Gv) bytes, the same
 //      total as the canonical [t][g][(s, z)] order.  pos = tau^-1 puts the 8
 //      tokens of K-group kg (lanes 16*kg .. 16*kg + 15) in 16 contiguous bytes,
 //      in B-fragment element order.
 //    key meta is [group][s[128], z[128]] in both layouts.
-//    4- and 8-bit codes (the b = 4 and 8 variants of the above) are not split
-//      into bit planes: a dword holds whole codes, 32/b fields of b bits, so
-//      that the codes of one MFMA operand become its halves with one
-//      instruction per pair.  Field f of a dword holds operand element
-//      e = field_elem(f, b): b = 8, dword h of an 8-element operand holds
-//      elements 4h + f at byte f; b = 4, the operand's single dword holds
-//      element pair i at nibbles (i, i + 4).
-//      keys: channel c = 32*kb + 8*g + e sits in row dword (b/4)*(4*g + kb)
-//        + (b == 8 ? e >> 2 : 0);
-//      values: lane L holds 2*b dwords, channel block mb in dwords
-//        (b/4)*mb + (b == 8 ? e' >> 2 : 0) of the lane, e' as above.
 #pragma once
 
 #include <stdint.h>
@@ -59,45 +60,76 @@ struct BitLoc {
   int bit;
 };
 
-// Whole-code (4- and 8-bit) operand layout: the dword (within the operand's
-// b/4 dwords) and field of operand element e (0..7), and its inverse.
+// Dword (within the operand's dwords) and bit offset of element e (0..7)
+// of a whole-code operand at 4 or 8 bits; field_elem inverts it.
 KVQ_HD inline int elem_word(int e, int b) { return b == 8 ? e >> 2 : 0; }
 KVQ_HD inline int elem_field(int e, int b) { return b == 8 ? e & 3 : (e >> 1) + 4 * (e & 1); }
 KVQ_HD inline int field_elem(int w, int f, int b) { return b == 8 ? 4 * w + f : 2 * (f & 3) + (f >> 2); }
 
-// Key code bit of channel c, plane p (matrix layout).
+// Key code bit p of channel c (matrix layout): dword within the row, bit.
 KVQ_HD inline BitLoc key_bit(int c, int p, int b) {
   const int kb = c >> 5, g = (c >> 3) & 3, e = c & 7;
-  if (b <= 2) return {g * b + p, pair_bit(kb, e)};
+  if (b == 1) return {g, pair_bit(kb, e)};
+  if (b == 2) return {2 * g + (kb >> 1), 8 * (kb & 1) + 2 * (e >> 1) + 16 * (e & 1) + p};
   return {(b / 4) * (4 * g + kb) + elem_word(e, b), b * elem_field(e, b) + p};
 }
 
-// Channel of field f of key row dword w (whole-code layouts).
-KVQ_HD inline int key_field_channel(int w, int f, int b) {
-  const int q = w / (b / 4), g = q >> 2, kb = q & 3;
-  return 32 * kb + 8 * g + field_elem(w % (b / 4), f, b);
+// The channel and code bit that key row dword w, bit q holds.
+KVQ_HD inline void key_bit_owner(int w, int q, int b, int& c, int& p) {
+  int g, kb, e;
+  if (b == 1) {
+    g = w;
+    kb = 2 * ((q >> 3) & 1) + ((q >> 2) & 1);
+    e = 2 * (q & 3) + (q >> 4);
+    p = 0;
+  } else if (b == 2) {
+    g = w >> 1;
+    kb = 2 * (w & 1) + ((q >> 3) & 1);
+    e = 2 * ((q >> 1) & 3) + (q >> 4);
+    p = q & 1;
+  } else {
+    const int o = w / (b / 4);  // = 4*g + kb
+    g = o >> 2;
+    kb = o & 3;
+    e = field_elem(w % (b / 4), q / b, b);
+    p = q % b;
+  }
+  c = 32 * kb + 8 * g + e;
 }
-
-// Bit of value-operand element e' (0..7) of channel block m4 (0..3) in its dword.
-KVQ_HD inline int value_elem_bit(int m4, int e) { return 8 * m4 + e; }
 
 // Block token of value-operand element e' of K-group kg.
 KVQ_HD inline int value_token(int kg, int e) { return e < 4 ? 4 * kg + e : 16 + 4 * kg + (e - 4); }
 
-// Value code bit of block token r (0..31), channel c, plane p.
+// Value code bit p of block token r (0..31), channel c (matrix layout):
+// dword within the 32-token block, bit.
 KVQ_HD inline BitLoc value_bit(int r, int c, int p, int b) {
   const int hi = r >> 4, r16 = r & 15;
   const int kg = r16 >> 2, e = (r16 & 3) + 4 * hi;
-  const int mb = c >> 4, d = mb >> 2, m4 = mb & 3;
+  const int mb = c >> 4;
   const int lane = (c & 15) + 16 * kg;
-  if (b <= 2) return {lane * 2 * b + d * b + p, value_elem_bit(m4, e)};
+  if (b == 1) return {lane * 2 + (mb >> 2), 8 * (mb & 3) + e};
+  if (b == 2) return {lane * 4 + (mb >> 1), 16 * (mb & 1) + 2 * e + p};
   return {lane * 2 * b + (b / 4) * mb + elem_word(e, b), b * elem_field(e, b) + p};
 }
 
-// Block token and channel of field f of value block dword w (whole-code layouts).
-KVQ_HD inline void value_field_loc(int w, int f, int b, int& r, int& c) {
-  const int lane = w / (2 * b), q = w % (2 * b), mb = q / (b / 4);
-  r = value_token(lane >> 4, field_elem(q % (b / 4), f, b));
+// The block token, channel and code bit that value block dword w, bit q holds.
+KVQ_HD inline void value_bit_owner(int w, int q, int b, int& r, int& c, int& p) {
+  const int lane = w / (2 * b), o = w % (2 * b);
+  int mb, e;
+  if (b == 1) {
+    mb = 4 * o + (q >> 3);
+    e = q & 7;
+    p = 0;
+  } else if (b == 2) {
+    mb = 2 * o + (q >> 4);
+    e = (q >> 1) & 7;
+    p = q & 1;
+  } else {
+    mb = o / (b / 4);
+    e = field_elem(o % (b / 4), q / b, b);
+    p = q % b;
+  }
+  r = value_token(lane >> 4, e);
   c = 16 * mb + (lane & 15);
 }
 
