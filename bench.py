@@ -41,7 +41,9 @@ def packed_bytes(L: int, w, bk: int, bv: int) -> int:
 
 def matrix_path(w) -> bool:
     """Whether the library decodes this workload on the matrix cores."""
-    return (w.group_q == 4 and w.bits_k[0] in (1, 2) and w.bits_v[0] in (1, 2) and w.value_group >= 32)
+    bk, bv = w.bits_k[0], w.bits_v[0]
+    bits = (bk in (1, 2) and bv in (1, 2)) or (bk == bv and bk in (4, 8))
+    return w.group_q in (4, 5, 8) and bits and w.value_group >= 32
 
 
 def source_digest() -> str:
@@ -358,7 +360,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.key_group // 32}>" if matrix_path(w) else
+            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.key_group // 32},{w.group_q}>" if matrix_path(w) else
                        f"decode_split_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.group_q}>"),
             "bytes_per_launch": launch_bytes,
             "kernel_source_sha256_16": source_digest(),
