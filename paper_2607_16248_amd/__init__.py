@@ -1,6 +1,7 @@
 """Packed low-bit KV cache and single-token decode attention for MI355X (gfx950).
 
-The computation lives in the HIP library libkvq.so (C ABI: include/kvq.h);
+The computation lives in the HIP library libkvq.so (C ABI: include/kvq.h and
+include/dgap.h, DGAP's logit-side step);
 :mod:`paper_2607_16248_amd.kvq` is its thin ctypes binding.
 """
 from .kvq import (KVCache, KvqError, kvq_append, kvq_append_decode, kvq_cache_bytes, kvq_cache_destroy,  # noqa: F401
@@ -8,3 +9,4 @@ from .kvq import (KVCache, KvqError, kvq_append, kvq_append_decode, kvq_cache_by
                   kvq_decode_merge, kvq_decode_partials, kvq_dequant,
                   kvq_export, kvq_export_bytes, kvq_last_error, kvq_seq_len, kvq_set_split_tokens,
                   kvq_version, kvq_workspace_bytes, make_desc)
+from .kvq import dgap_info_floats, dgap_params, dgap_restore, dgap_workspace_bytes  # noqa: F401

@@ -30,6 +30,7 @@ SOURCES = [
     ("decode.hip", ["-fno-honor-nans"]),
     ("decode_mfma.hip", ["-fno-honor-nans"]),
     ("dequant.hip", []),
+    ("dgap.hip", []),
     ("kvq_api.cpp", []),
 ]
 

@@ -16,6 +16,7 @@
 #include <utility>
 #include <vector>
 
+#include "dgap.h"
 #include "kvq.h"
 #include "kvq_internal.h"
 
@@ -612,6 +613,59 @@ kvq_status kvq_set_split_tokens(kvq_cache* c, int32_t tokens) {
   if (tokens > 0 && (c->cq + tokens - 1) / tokens > kMaxSplits)
     return fail(KVQ_ERR_ARG, "split tokens %d would give more than %d splits at capacity", tokens, kMaxSplits);
   c->split_tokens = tokens;
+  return ok();
+}
+
+// ------------------------------------------------------------------ DGAP
+
+size_t dgap_workspace_bytes(int32_t batch, int32_t vocab, int32_t k) {
+  if (batch < 1 || k < DGAP_MIN_K || k > DGAP_MAX_K || vocab < k || vocab > (1 << 24)) return 0;
+  const int64_t nchunk = (vocab + kvq::kDgapChunk - 1) / kvq::kDgapChunk;
+  if (nchunk * k > kvq::kDgapMaxCandidates) return 0;
+  const uint64_t stats = ((uint64_t)batch * nchunk * 4 * sizeof(float) + kvq::kAlign - 1) / kvq::kAlign * kvq::kAlign;
+  return (size_t)(stats + (uint64_t)batch * nchunk * k * sizeof(uint64_t));
+}
+
+size_t dgap_info_floats(int32_t k) { return (size_t)kvq::kDgapInfoHead + 2 * (size_t)(k > 0 ? k : 0); }
+
+kvq_status dgap_restore(const dgap_params* p, float* logits, int32_t batch, void* ws, size_t ws_bytes, float* info,
+                        void* stream) {
+  if (!p) return fail(KVQ_ERR_ARG, "params is NULL");
+  if (batch < 1) return fail(KVQ_ERR_ARG, "batch must be >= 1 (got %d)", batch);
+  if (p->k < DGAP_MIN_K || p->k > DGAP_MAX_K)
+    return fail(KVQ_ERR_ARG, "k = %d outside [%d, %d]", p->k, DGAP_MIN_K, DGAP_MAX_K);
+  if (p->vocab < p->k) return fail(KVQ_ERR_ARG, "vocab %d smaller than k %d", p->vocab, p->k);
+  if (p->hidden_det < 1 || p->hidden_det > DGAP_MAX_HIDDEN || p->hidden_corr < 1 || p->hidden_corr > DGAP_MAX_HIDDEN)
+    return fail(KVQ_ERR_ARG, "hidden sizes (%d, %d) outside [1, %d]", p->hidden_det, p->hidden_corr, DGAP_MAX_HIDDEN);
+  if (!(p->tau == p->tau)) return fail(KVQ_ERR_ARG, "tau is NaN");
+  if (!p->det_w1 || !p->det_b1 || !p->det_w2 || !p->corr_w1 || !p->corr_b1 || !p->corr_w2)
+    return fail(KVQ_ERR_ARG, "a weight pointer is NULL");
+  if (!logits) return fail(KVQ_ERR_ARG, "logits is NULL");
+  const size_t need = dgap_workspace_bytes(batch, p->vocab, p->k);
+  if (need == 0)
+    return fail(KVQ_ERR_UNSUPPORTED, "vocab %d with k %d: at most 2^24 logits and %d window candidates per row",
+                p->vocab, p->k, kvq::kDgapMaxCandidates);
+  if (!ws) return fail(KVQ_ERR_ARG, "workspace is NULL");
+  if (ws_bytes < need) return fail(KVQ_ERR_CAPACITY, "workspace holds %zu bytes, this call needs %zu", ws_bytes, need);
+  if (reinterpret_cast<uintptr_t>(ws) % 16 != 0) return fail(KVQ_ERR_ARG, "workspace must be 16-byte aligned");
+  kvq::DgapArgs a{};
+  a.logits = logits;
+  a.info = info;
+  a.vocab = p->vocab;
+  a.k = p->k;
+  a.nchunk = (p->vocab + kvq::kDgapChunk - 1) / kvq::kDgapChunk;
+  a.hidden_det = p->hidden_det;
+  a.hidden_corr = p->hidden_corr;
+  a.tau = p->tau;
+  a.det_b2 = p->det_b2;
+  a.corr_b2 = p->corr_b2;
+  a.det_w1 = p->det_w1; a.det_b1 = p->det_b1; a.det_w2 = p->det_w2;
+  a.corr_w1 = p->corr_w1; a.corr_b1 = p->corr_b1; a.corr_w2 = p->corr_w2;
+  const uint64_t stats = ((uint64_t)batch * a.nchunk * 4 * sizeof(float) + kvq::kAlign - 1) / kvq::kAlign * kvq::kAlign;
+  a.ws_stats = static_cast<float*>(ws);
+  a.ws_cand = reinterpret_cast<uint64_t*>(static_cast<uint8_t*>(ws) + stats);
+  const int e = kvq::launch_dgap(a, batch, stream);
+  if (e) return hip_fail(e, "dgap launch");
   return ok();
 }
 

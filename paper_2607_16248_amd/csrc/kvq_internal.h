@@ -112,6 +112,30 @@ struct MergeArgs {
   MergeSeq seq[kMaxSeqPerLaunch];
 };
 
+// ---------------------------------------------------------------- DGAP
+
+constexpr int kDgapChunk = 2048;            // logits per scan workgroup
+constexpr int kDgapMaxK = 256;              // largest window
+constexpr int kDgapMaxCandidates = 32768;   // chunks * K per row, held by one workgroup
+constexpr int kDgapFeatures = 12;
+constexpr int kDgapCandInputs = 5;
+constexpr int kDgapInfoHead = 16;           // info floats before the window's indices
+
+struct DgapArgs {
+  float* logits;       // [batch][vocab], corrected in place
+  float* info;         // [batch][kDgapInfoHead + 2k] or null
+  float* ws_stats;     // [batch][nchunk][4]: chunk max m, sum e, sum (m - z) e, sum e^2 (e = e^(z - m))
+  uint64_t* ws_cand;   // [batch][nchunk][k] candidate keys (0 = empty)
+  const float* det_w1;
+  const float* det_b1;
+  const float* det_w2;
+  const float* corr_w1;
+  const float* corr_b1;
+  const float* corr_w2;
+  int32_t vocab, k, nchunk, hidden_det, hidden_corr;
+  float tau, det_b2, corr_b2;
+};
+
 // ---------------------------------------------------------------- dequant
 
 struct DequantArgs {
@@ -150,6 +174,7 @@ bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes
 int matrix_decode_occupancy(int bk, int bv, int gk, int gq);
 int launch_export(const ExportArgs& a, void* stream);
 int launch_merge(const MergeArgs& a, void* stream);
+int launch_dgap(const struct DgapArgs& a, int batch, void* stream);
 int launch_dequant(const DequantArgs& a, void* stream);
 int launch_fill_zero(void* dst, size_t words, void* stream);
 

@@ -22,7 +22,8 @@ EXPORTED = ["kvq_cache_bytes", "kvq_cache_init", "kvq_cache_destroy", "kvq_cache
             "kvq_seq_len", "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention", "kvq_append_decode",
             "kvq_decode_partials", "kvq_decode_merge",
             "kvq_dequant", "kvq_export_bytes", "kvq_export", "kvq_check",
-            "kvq_set_split_tokens", "kvq_last_error", "kvq_version"]
+            "kvq_set_split_tokens", "kvq_last_error", "kvq_version",
+            "dgap_workspace_bytes", "dgap_info_floats", "dgap_restore"]
 
 
 class KvqError(RuntimeError):
@@ -38,6 +39,15 @@ class CacheDesc(ctypes.Structure):
                 ("max_tokens", ctypes.c_int32), ("key_group", ctypes.c_int32),
                 ("value_group", ctypes.c_int32), ("fp16_window", ctypes.c_int32),
                 ("bits_k", ctypes.POINTER(ctypes.c_uint8)), ("bits_v", ctypes.POINTER(ctypes.c_uint8))]
+
+
+class DgapParams(ctypes.Structure):
+    """dgap_params of include/dgap.h (weights are device pointers)."""
+    _fields_ = [("vocab", ctypes.c_int32), ("k", ctypes.c_int32), ("hidden_det", ctypes.c_int32),
+                ("hidden_corr", ctypes.c_int32), ("tau", ctypes.c_float), ("det_b2", ctypes.c_float),
+                ("corr_b2", ctypes.c_float), ("pad", ctypes.c_int32),
+                ("det_w1", ctypes.c_void_p), ("det_b1", ctypes.c_void_p), ("det_w2", ctypes.c_void_p),
+                ("corr_w1", ctypes.c_void_p), ("corr_b1", ctypes.c_void_p), ("corr_w2", ctypes.c_void_p)]
 
 
 _lib = None
@@ -73,6 +83,9 @@ def lib():
         "kvq_set_split_tokens": ([P, I32], ctypes.c_int),
         "kvq_last_error": ([], ctypes.c_char_p),
         "kvq_version": ([], ctypes.c_char_p),
+        "dgap_workspace_bytes": ([I32, I32, I32], S),
+        "dgap_info_floats": ([I32], S),
+        "dgap_restore": ([ctypes.POINTER(DgapParams), P, I32, P, S, P, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -302,3 +315,31 @@ class KVCache:
 
     def reset(self):
         kvq_cache_reset(self.handle)
+
+
+# ------------------------------------------------------------------ DGAP
+
+def dgap_workspace_bytes(batch: int, vocab: int, k: int) -> int:
+    return int(lib().dgap_workspace_bytes(batch, vocab, k))
+
+
+def dgap_info_floats(k: int) -> int:
+    return int(lib().dgap_info_floats(k))
+
+
+def dgap_params(vocab: int, k: int, tau: float, det_w1, det_b1, det_w2, det_b2: float,
+                corr_w1, corr_b1, corr_w2, corr_b2: float) -> DgapParams:
+    """Params from device fp32 tensors (det_w1 [12][hd], corr_w1 [17][hc], ...)."""
+    return DgapParams(int(vocab), int(k), int(det_b1.numel()) if det_b1 is not None else 0,
+                      int(corr_b1.numel()) if corr_b1 is not None else 0, float(tau), float(det_b2),
+                      float(corr_b2), 0, _ptr(det_w1), _ptr(det_b1), _ptr(det_w2), _ptr(corr_w1),
+                      _ptr(corr_b1), _ptr(corr_w2))
+
+
+def dgap_restore(params: DgapParams, logits, batch: int, ws, ws_bytes: Optional[int] = None, info=None,
+                 stream=None) -> None:
+    """One DGAP step on ``batch`` rows of device fp32 logits, in place."""
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().dgap_restore(ctypes.byref(params), _ptr(logits), int(batch), _ptr(ws), int(ws_bytes),
+                              _ptr(info), _stream(stream)))

@@ -1,6 +1,6 @@
 """Host-side tests of the C-ABI library (no GPU needed).
 
-The library loads, exports every function include/kvq.h declares, sizes its
+The library loads, exports every function include/*.h declares, sizes its
 arena as documented, and rejects bad arguments before touching any device
 memory, leaving the cache unchanged.
 """
@@ -16,15 +16,20 @@ FAKE_ARENA = 1 << 30   # a 256-aligned address that is never dereferenced on the
 
 
 def declared_functions():
-    src = open(os.path.join(ROOT, "include", "kvq.h")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(kvq_[a-z_]+)\s*\(", src)))
+    names = set()
+    for h in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if not h.endswith(".h"):
+            continue
+        src = open(os.path.join(ROOT, "include", h)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        names |= set(re.findall(r"\b((?:kvq|dgap)_[a-z_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_library_exports_every_declared_function():
     lib = kvq.lib()
     names = declared_functions()
-    assert len(names) >= 15
+    assert len(names) >= 18
     for n in names:
         assert hasattr(lib, n), n
     assert sorted(names) == sorted(kvq.EXPORTED)
@@ -183,3 +188,43 @@ def test_split_setting_and_workspace_bound():
         assert e.value.status == kvq.ERR_ARG
     finally:
         kvq.kvq_cache_destroy(h)
+
+
+def test_dgap_sizes_and_argument_errors():
+    """dgap_restore checks every argument before it launches anything."""
+    # workspace: chunk statistics (256-byte aligned) + one 8-byte key per window slot per chunk
+    assert kvq.dgap_workspace_bytes(1, 152064, 128) == align(75 * 16) + 75 * 128 * 8
+    assert kvq.dgap_workspace_bytes(4, 128256, 64) == align(4 * 63 * 16) + 4 * 63 * 64 * 8
+    assert kvq.dgap_workspace_bytes(1, 100, 4) == 0            # k below 8
+    assert kvq.dgap_workspace_bytes(1, 100, 200) == 0          # vocab below k
+    assert kvq.dgap_workspace_bytes(1, 1 << 20, 256) == 0      # 512 chunks x 256 > 32768 candidates
+    assert kvq.dgap_info_floats(128) == 16 + 256
+    F = FAKE_ARENA
+
+    def params(**kw):
+        d = dict(vocab=32768, k=32, tau=0.6)
+        d.update(kw)
+        p = kvq.DgapParams(d["vocab"], d["k"], kw.get("hd", 32), kw.get("hc", 32), d["tau"], 0.0, 0.0, 0,
+                           F, F, F, F, F, kw.get("cw2", F))
+        return p
+
+    ws_ok = kvq.dgap_workspace_bytes(1, 32768, 32)
+    cases = [
+        (params(k=4), ws_ok, F, kvq.ERR_ARG),
+        (params(k=300), ws_ok, F, kvq.ERR_ARG),
+        (params(vocab=16, k=32), ws_ok, F, kvq.ERR_ARG),
+        (params(hd=0), ws_ok, F, kvq.ERR_ARG),
+        (params(hc=65), ws_ok, F, kvq.ERR_ARG),
+        (params(cw2=None), ws_ok, F, kvq.ERR_ARG),
+        (params(tau=float("nan")), ws_ok, F, kvq.ERR_ARG),
+        (params(vocab=(1 << 24) + 1, k=8), 1 << 30, F, kvq.ERR_UNSUPPORTED),
+        (params(), ws_ok - 8, F, kvq.ERR_CAPACITY),
+        (params(), ws_ok, F + 8, kvq.ERR_ARG),
+    ]
+    for p, wsb, wsp, status in cases:
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.dgap_restore(p, F, 1, wsp, ws_bytes=wsb, stream=0)
+        assert e.value.status == status, (p.k, p.vocab, wsb, status)
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.dgap_restore(params(), F, 0, F, ws_bytes=ws_ok, stream=0)
+    assert e.value.status == kvq.ERR_ARG
