@@ -10,6 +10,9 @@ Inputs are synthetic and resident in HBM before timing; the 32 caches
 
 Prints ONE JSON line.  value = packed-KV bytes the decode kernels must read
 per step (codes + fp16 scales/zeros + fp16 tail, all layers) / step time.
+The line also carries "dgap": DGAP's logit-side step (features, detector,
+top-K window, corrector, merge) on one logit row of the workload's model
+vocabulary, timed on its own (--no-dgap skips it).
 """
 from __future__ import annotations
 
@@ -110,6 +113,70 @@ def cpu_baseline(w, kv_heads: int):
     }
 
 
+# DGAP window sizes K_b per KbVb precision (a reading: the paper calibrates
+# them from traces; lower bits, larger windows) and the vocabulary of each
+# workload's model.
+DGAP_K = {1: 128, 2: 64, 4: 32, 8: 16}
+DGAP_VOCAB = {0: ("llama3_8b", 128256), 1: ("llama3_8b", 128256), 2: ("llama3_8b", 128256),
+              3: ("mistral_7b", 32768), 4: ("qwen2_5_14b", 152064)}
+
+
+def dgap_leg(workload_idx: int, bits: int, iters: int):
+    """DGAP's logit-side step after each decode step: one batch-1 logit row of
+    the workload's vocabulary, timed back to back with HIP events on the
+    launch stream, once with a detector that always corrects and once with one
+    that never does."""
+    import torch
+
+    from dgap_inputs import gen_logits, gen_weights
+    from paper_2607_16248_amd import kvq
+
+    dev = torch.device("cuda:0")
+    model, V = DGAP_VOCAB[workload_idx]
+    k = DGAP_K[bits]
+    stream = torch.cuda.current_stream().cuda_stream
+    z0 = gen_logits(V, 1, seed=0)
+    out = {"model_vocab": model, "vocab": V, "k": k, "tau": 0.6, "batch": 1}
+    for name, bias in (("corrected", 20.0), ("bypass", -20.0)):
+        w = gen_weights(0, det_bias=bias)
+        t = {n: torch.from_numpy(getattr(w, n)).to(dev) for n in ("w1", "b1", "w2", "c1", "cb1", "c2")}
+        p = kvq.dgap_params(V, k, 0.6, t["w1"], t["b1"], t["w2"], w.b2, t["c1"], t["cb1"], t["c2"], w.cb2)
+        z = torch.from_numpy(z0).to(dev)
+        ws = torch.empty(kvq.dgap_workspace_bytes(1, V, k), dtype=torch.uint8, device=dev)
+        for _ in range(8):
+            kvq.dgap_restore(p, z, 1, ws, stream=stream)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(iters):
+            kvq.dgap_restore(p, z, 1, ws, stream=stream)
+        b.record()
+        torch.cuda.synchronize()
+        out[f"us_{name}"] = round(a.elapsed_time(b) * 1e3 / iters, 3)
+    # bytes one call must move: the row (read once) and the chunk partials
+    nchunk = -(-V // 2048)
+    out["bytes_per_call"] = V * 4 + nchunk * (16 + 8 * k) * 2 + 2 * k * 4
+    out["gbs_corrected"] = round(out["bytes_per_call"] / (out["us_corrected"] * 1e-6) / 1e9, 2)
+    out["bound"] = "latency (two dependent launches; the row is 0.5-0.6 MB)"
+    return out
+
+
+def dgap_cpu_baseline(workload_idx: int, bits: int) -> float:
+    """Part of the CPU-baseline leg: the DGAP oracle (fp64, one thread) on the
+    same row, microseconds per corrected step."""
+    from dgap_inputs import gen_logits, gen_weights
+    from oracle import dgap as odgap
+
+    _, V = DGAP_VOCAB[workload_idx]
+    z0 = gen_logits(V, 1, seed=0)[0]
+    w = gen_weights(0, det_bias=20.0)
+    reps = 5
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        odgap.restore(z0, DGAP_K[bits], w)
+    return round((time.perf_counter() - t0) * 1e6 / reps, 1)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -120,6 +187,7 @@ def main():
     ap.add_argument("--kernel-iters", type=int, default=256)
     ap.add_argument("--cpu-heads", type=int, default=4, help="kv heads in the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dgap", action="store_true", help="skip the DGAP logit-side leg")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="end with 4 plain device copies of 256 MiB (counter calibration)")
     args = ap.parse_args()
@@ -373,9 +441,14 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if not args.no_dgap:
+        log("[bench] DGAP logit-side step")
+        result["dgap"] = dgap_leg(args.workload, w.bits_k[0], 200)
     if not args.no_cpu_baseline:
         log("[bench] CPU baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(w, min(args.cpu_heads, w.num_kv_heads))
+        if not args.no_dgap:
+            result["cpu_baseline"]["dgap_oracle_us_per_step"] = dgap_cpu_baseline(args.workload, w.bits_k[0])
     else:
         result["cpu_baseline"] = None
     print(json.dumps(result), flush=True)

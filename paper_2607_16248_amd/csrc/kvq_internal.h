@@ -120,6 +120,7 @@ constexpr int kDgapMaxCandidates = 32768;   // chunks * K per row, held by one w
 constexpr int kDgapFeatures = 12;
 constexpr int kDgapCandInputs = 5;
 constexpr int kDgapInfoHead = 16;           // info floats before the window's indices
+constexpr int kDgapMaxHidden = 64;
 
 struct DgapArgs {
   float* logits;       // [batch][vocab], corrected in place
