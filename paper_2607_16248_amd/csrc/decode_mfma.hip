@@ -525,9 +525,11 @@ decode_mfma_kernel(DecodeArgs a) {
 
     // online softmax (base 2) per head over these 32 tokens; cs > 0, so the
     // maximum is taken before scaling.  The reference m moves only when a
-    // score exceeds it, and then to kLazyMargin above that score: every
-    // weight stays <= 1, and the rescale of the accumulators (and its
-    // exponential) is skipped while later maxima stay under the reference.
+    // score exceeds it, and then to kLazyMargin above the block maximum of
+    // the head: every weight stays <= 1, and the rescale of the accumulators
+    // (and its exponential) is skipped while later scores stay under the
+    // reference.  Each lane compares its own two scores; only a block with a
+    // score above its reference reduces the maxima across the row's lanes.
     // With a weight shift (PShift) m and every score are kept kPShift lower,
     // so the weights reach 2^kPShift; m is the reference of the record.
     const float ninf = -__builtin_inff();
@@ -535,11 +537,7 @@ decode_mfma_kernel(DecodeArgs a) {
     bool up = false;
 #pragma unroll
     for (int hh = 0; hh < HPL; ++hh) {
-      float b = fmaxf(raw[hh][0], raw[hh][1]);
-      b = fmaxf(b, dpp_mov<kQuadXor1>(ninf, b));
-      b = fmaxf(b, dpp_mov<kQuadXor2>(ninf, b));
-      b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
-      b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
+      const float b = fmaxf(raw[hh][0], raw[hh][1]);
       bm[hh] = kPShift ? fmaf(b, cs[hh], -(float)kPShift) : b * cs[hh];
       up |= bm[hh] > m[hh];
     }
@@ -547,7 +545,12 @@ decode_mfma_kernel(DecodeArgs a) {
       float alpha[HPL];
 #pragma unroll
       for (int hh = 0; hh < HPL; ++hh) {
-        const float mnew = bm[hh] > m[hh] ? bm[hh] + kLazyMargin : m[hh];
+        float b = bm[hh];  // scaling by cs > 0 (and the shift) keeps the order
+        b = fmaxf(b, dpp_mov<kQuadXor1>(ninf, b));
+        b = fmaxf(b, dpp_mov<kQuadXor2>(ninf, b));
+        b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
+        b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
+        const float mnew = b > m[hh] ? b + kLazyMargin : m[hh];
         alpha[hh] = __builtin_amdgcn_exp2f(m[hh] - mnew);  // 1 where the reference stays
         l[hh] *= alpha[hh];
         m[hh] = mnew;
