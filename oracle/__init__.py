@@ -164,6 +164,50 @@ def attention(q, Khat: np.ndarray, Vhat: np.ndarray, return_weights: bool = Fals
     return out
 
 
+def chunk_attention(q, Khat: np.ndarray, Vhat: np.ndarray):
+    """fp64 attention of the last n_q positions of a cache, causal among them.
+
+    Chunked prefill and the verification step of speculative decoding
+    (Related Work) evaluate several consecutive query positions at once;
+    each is the scaled dot-product attention of the decoder (Introduction)
+    over the cache up to and including its own position.  q fp16
+    [n_q][Hq][d]; Khat, Vhat fp64 [Hkv][L][d] with L >= n_q.  Query i is
+    position L - n_q + i and attends to tokens [0, L - n_q + i]: the
+    decode attention above on that prefix.
+    """
+    qu = _as_u16(q)
+    n_q = qu.shape[0]
+    L = Khat.shape[1]
+    if not 1 <= n_q <= L:
+        raise OracleError(ERR_ARG, "chunk_attention: need 1 <= n_q <= L")
+    out = np.zeros((n_q,) + qu.shape[1:], dtype=np.float64)
+    for i in range(n_q):
+        visible = L - n_q + 1 + i
+        out[i] = attention(qu[i], Khat[:, :visible], Vhat[:, :visible])
+    return out
+
+
+def chunk_seq(q, K, V, bits_k: int, bits_v: int, key_group: int, value_group: int,
+              window: int, heads: Optional[List[int]] = None):
+    """Quantize one sequence's cache, dequantize it and run chunk_attention.
+
+    q fp16 [n_q][Hq][d]; K, V fp16 [L][Hkv][d].  Rows of kv heads outside
+    ``heads`` are left NaN.
+    """
+    qu = _as_u16(q)
+    L, Hkv, d = K.shape
+    n_q, Hq = qu.shape[0], qu.shape[1]
+    gq = Hq // Hkv
+    heads = list(range(Hkv)) if heads is None else list(heads)
+    out = np.full((n_q, Hq, d), np.nan)
+    for h in heads:
+        img = build_head(np.ascontiguousarray(K[:, h, :]), np.ascontiguousarray(V[:, h, :]),
+                         bits_k, bits_v, key_group, value_group, window)
+        Kh, Vh = dequant_head(img, L, d, bits_k, bits_v, key_group, value_group, window)
+        out[:, h * gq:(h + 1) * gq] = chunk_attention(qu[:, h * gq:(h + 1) * gq], Kh[None], Vh[None])
+    return out
+
+
 def decode_seq(q, K, V, bits_k: int, bits_v: int, key_group: int, value_group: int,
                window: int, heads: Optional[List[int]] = None):
     """Quantize one sequence's cache, dequantize it and attend.

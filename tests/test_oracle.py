@@ -383,3 +383,49 @@ def test_decode_seq_pipeline_consistent():
         Khs.append(Kh)
         Vhs.append(Vh)
     np.testing.assert_allclose(out, _sdpa_ref(q, np.stack(Khs), np.stack(Vhs)), rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------- chunk queries (causal)
+
+@pytest.mark.parametrize("L,n_q,d,Hq,Hkv", [(1, 1, 8, 1, 1), (5, 5, 8, 4, 1), (33, 7, 128, 4, 1),
+                                            (65, 16, 128, 8, 2), (40, 3, 128, 10, 2)])
+def test_chunk_attention_matches_masked_sdpa(L, n_q, d, Hq, Hkv):
+    # torch SDPA over all n_q queries at once with an explicit boolean mask
+    # (query i sees tokens t <= L - n_q + i): a different formulation
+    rng = np.random.default_rng([L, n_q, d, Hq])
+    q = rng.standard_normal((n_q, Hq, d)).astype(np.float16)
+    Kh = rng.standard_normal((Hkv, L, d)) * 2
+    Vh = rng.standard_normal((Hkv, L, d))
+    out = oracle.chunk_attention(q, Kh, Vh)
+    qt = torch.from_numpy(q.astype(np.float64)).permute(1, 0, 2).unsqueeze(0)     # [1][Hq][n_q][d]
+    k = torch.from_numpy(Kh).repeat_interleave(Hq // Hkv, dim=0).unsqueeze(0)     # [1][Hq][L][d]
+    v = torch.from_numpy(Vh).repeat_interleave(Hq // Hkv, dim=0).unsqueeze(0)
+    mask = torch.arange(L)[None, :] <= (L - n_q + torch.arange(n_q))[:, None]
+    ref = torch.nn.functional.scaled_dot_product_attention(qt, k, v, attn_mask=mask)
+    np.testing.assert_allclose(out, ref[0].permute(1, 0, 2).numpy(), rtol=1e-12, atol=1e-13)
+
+
+def test_chunk_attention_causality_and_end_cases():
+    rng = np.random.default_rng(12)
+    d, L, n_q, Hq, Hkv = 128, 60, 9, 8, 2
+    q = rng.standard_normal((n_q, Hq, d)).astype(np.float16)
+    Kh = rng.standard_normal((Hkv, L, d)) * 3
+    Vh = rng.standard_normal((Hkv, L, d))
+    base = oracle.chunk_attention(q, Kh, Vh)
+    # the last query sees the whole cache: plain decode attention
+    assert (base[-1] == oracle.attention(q[-1], Kh, Vh)).all()
+    # a token past a query's position changes nothing for that query, and
+    # changes every query that sees it
+    t = L - n_q + 4
+    K2, V2 = Kh.copy(), Vh.copy()
+    K2[:, t] += 5.0
+    V2[:, t] -= 7.0
+    pert = oracle.chunk_attention(q, K2, V2)
+    assert (pert[:4] == base[:4]).all()
+    assert all(np.abs(pert[i] - base[i]).max() > 1e-6 for i in range(4, n_q))
+    # n_q = L: the first query sees only token 0, its output is that value row
+    qa = rng.standard_normal((L, Hq, d)).astype(np.float16)
+    full = oracle.chunk_attention(qa, Kh, Vh)
+    assert (full[0] == np.repeat(Vh[:, 0], Hq // Hkv, axis=0)).all()
+    with pytest.raises(oracle.OracleError):
+        oracle.chunk_attention(qa[:1].repeat(L + 1, 0), Kh, Vh)
