@@ -153,6 +153,35 @@ kvq_status kvq_decode_partials(const kvq_cache* cache, const void* q, void* ws, 
                                void* stream);
 kvq_status kvq_decode_merge(const kvq_cache* cache, const void* ws, float* out, void* stream);
 
+/* Most queries per sequence in one kvq_chunk_attention call. */
+#define KVQ_MAX_CHUNK 1024
+
+/* Workspace bytes kvq_chunk_attention needs for n_q queries per sequence
+ * (n_q times kvq_workspace_bytes); 0 if n_q is outside [1, KVQ_MAX_CHUNK]. */
+size_t kvq_chunk_workspace_bytes(const kvq_cache* cache, int32_t n_q);
+
+/* Attention of the last n_q tokens of every sequence over its cache, causal
+ * among them: the same scaled dot-product attention as
+ * kvq_decode_attention, for the several query positions that chunked
+ * prefill and the verification step of speculative decoding evaluate at
+ * once (Related Work: paged serving and I/O-aware attention kernels; the
+ * quantized caches built for speculative decoding).  Query i of sequence s
+ * is the token at position L_s - n_q + i (already appended) and attends to
+ * tokens [0, L_s - n_q + i]:
+ *   out[s][i][h][:] = softmax over t <= L_s - n_q + i of
+ *                     (q[s][i][h] . K^[s][kv(h)][t] / sqrt(d)) V^[s][kv(h)]
+ * q: device fp16 [batch][n_q][Hq][d]; out: device fp32 [batch][n_q][Hq][d];
+ * ws: device scratch of ws_bytes >= kvq_chunk_workspace_bytes(cache, n_q),
+ * 16-byte aligned, contents undefined on entry and exit.  Every sequence
+ * must hold at least n_q tokens.  With n_q = 1 the result equals
+ * kvq_decode_attention's.  The queries of a kv head are read in groups of
+ * up to 8 (query, head) rows, each group one pass over the cache.
+ * Errors: KVQ_ERR_ARG (n_q out of range, a sequence shorter than n_q, null
+ * pointers, misaligned workspace), KVQ_ERR_CAPACITY (workspace too small),
+ * KVQ_ERR_HIP. */
+kvq_status kvq_chunk_attention(const kvq_cache* cache, const void* q, int32_t n_q, float* out, void* ws,
+                               size_t ws_bytes, void* stream);
+
 /* Dequantize tokens [tok0, tok0 + ntok) of one sequence into device fp32
  * K_out, V_out [ntok][Hkv][d]: fmaf(code, s, z) for packed tokens (the
  * exact z + code*s rounded once to fp32) and the fp16 value for tail

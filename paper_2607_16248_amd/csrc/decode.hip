@@ -52,7 +52,8 @@ __device__ __forceinline__ uint64_t load_value8(const uint8_t* row, int cc) {
 template <int BK, int BV, int GQ>
 __device__ __forceinline__ void packed_group(const DecodeArgs& a, const uint8_t* blk, int j,
                                              const float (&qs0)[GQ], const float (&qs1)[GQ],
-                                             float* qp, float* p_lds, State<GQ>& st, int lane) {
+                                             float* qp, float* p_lds, State<GQ>& st, const int (&lim)[GQ],
+                                             int glim, int lane) {
   constexpr int QS = QStride<GQ>::value;
   // scales and zeros of the key group: this lane's channels 2*lane, 2*lane+1
   const uint32_t* km = reinterpret_cast<const uint32_t*>(blk + a.km + (size_t)j * 2 * kHeadDim * 2);
@@ -94,6 +95,11 @@ __device__ __forceinline__ void packed_group(const DecodeArgs& a, const uint8_t*
     }
 #pragma unroll
     for (int g = 0; g < GQ; ++g) sig[g] += dpp_mov<kQuadXor1>(0.f, sig[g]) + bias[g];
+    if (tbase + 32 > glim) {  // tokens past a chunk query's position
+#pragma unroll
+      for (int g = 0; g < GQ; ++g)
+        if (tbase + tl >= lim[g]) sig[g] = -__builtin_inff();
+    }
     softmax_pass<GQ>(st, sig, half, tl, p_lds);
     wave_lds_sync();
 
@@ -132,7 +138,7 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
 
   float qs0[GQ], qs1[GQ];
-  load_q_scaled<GQ>(a, S, wk.h, lane, qs0, qs1);
+  load_q_scaled<GQ>(a, S, wk.h, wk.rg, lane, qs0, qs1);
   State<GQ> st;
   init_state<GQ>(st);
 
@@ -141,14 +147,17 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   if (wk.sp < S.nq) {
     const int t0 = wk.sp * a.split_tokens;
     const int t1 = min(S.Lq, t0 + a.split_tokens);
+    int lim[GQ];
+    row_limits<GQ>(a, S, wk.h, wk.rg, lim);
+    const int glim = group_limit(a, S, wk.rg);
     for (int j = t0 / a.gk + wv; j < t1 / a.gk; j += kWaves)
-      packed_group<BK, BV, GQ>(a, blk, j, qs0, qs1, qp, pl, st, lane);
+      packed_group<BK, BV, GQ>(a, blk, j, qs0, qs1, qp, pl, st, lim, glim, lane);
   } else {
-    tail_split<GQ>(a, S, wk.h, blk, qs0, qs1, qp, pl, st, lane, wv);
+    tail_split<GQ>(a, S, wk.h, wk.rg, blk, qs0, qs1, qp, pl, st, lane, wv);
   }
   stage_state<GQ>(st, red, lane, wv);
   __syncthreads();
-  write_record<GQ>(a, S, wk.h, wk.sp, red);
+  write_record<GQ>(a, S, wk.h, wk.rg, wk.sp, red);
 }
 
 // One workgroup per (sequence, query head, 32-channel slice): thread
@@ -193,13 +202,17 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
 #pragma unroll
     for (int u = 0; u < kMergeUnroll; ++u)
       if (i0 + kMergeParts * u < n) mx = fmaxf(mx, mv[u]);
-    const float f = __builtin_amdgcn_exp2f(M - mx);  // M = -inf on the first batch: f = 0
+    // M = -inf on the first batch: f = 0.  A split that saw no token of a
+    // chunk query's row has m = -inf (l = 0, acc = 0); while every record so
+    // far is such a split, mx = -inf and nothing is added.
+    const bool none = mx == -__builtin_inff();
+    const float f = none ? 1.f : __builtin_amdgcn_exp2f(M - mx);
     D *= f;
     A *= f;
 #pragma unroll
     for (int u = 0; u < kMergeUnroll; ++u)
       if (i0 + kMergeParts * u < n) {
-        const float w = __builtin_amdgcn_exp2f(mv[u] - mx);
+        const float w = none ? 0.f : __builtin_amdgcn_exp2f(mv[u] - mx);
         D = fmaf(w, lv[u], D);
         A = fmaf(w, av[u], A);
       }
@@ -218,7 +231,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
     float den = 0.f, num = 0.f;
 #pragma unroll
     for (int p = 0; p < kMergeParts; ++p) {
-      const float w = __builtin_amdgcn_exp2f(sm[p] - mx);  // a part without splits has sm = -inf: w = 0
+      // a part without splits, or without a visible token, has sm = -inf:
+      // w = 0 (every row sees at least one token, so mx is finite)
+      const float w = __builtin_amdgcn_exp2f(sm[p] - mx);
       den = fmaf(w, sl[p], den);
       num = fmaf(w, sa[p][cs], num);
     }

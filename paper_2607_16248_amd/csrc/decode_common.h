@@ -81,8 +81,10 @@ __device__ __forceinline__ void softmax_pass(State<GQ>& st, float (&sig)[GQ], in
   for (int g = 0; g < GQ; ++g) {
     const float mx = wave_max(sig[g]);
     const float mnew = fmaxf(st.m[g], mx);
-    const float alpha = __builtin_amdgcn_exp2f(st.m[g] - mnew);
-    const float p = __builtin_amdgcn_exp2f(sig[g] - mnew);
+    // a row with no visible token yet keeps m = -inf: factor 1, weights 0
+    const bool none = mnew == -__builtin_inff();
+    const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(st.m[g] - mnew);
+    const float p = none ? 0.f : __builtin_amdgcn_exp2f(sig[g] - mnew);
     st.l[g] = st.l[g] * alpha + (half ? 0.f : p);
 #pragma unroll
     for (int k = 0; k < 8; ++k) st.acc[g][k] *= alpha;
@@ -95,7 +97,7 @@ __device__ __forceinline__ void softmax_pass(State<GQ>& st, float (&sig)[GQ], in
 template <int GQ>
 __device__ __forceinline__ void tail_pass(const DecodeArgs& a, const DecodeSeq& S, const uint8_t* blk,
                                           int pass, const float* qp, float* p_lds, State<GQ>& st,
-                                          int lane) {
+                                          const int (&lim)[GQ], int lane) {
   constexpr int QS = QStride<GQ>::value;
   const int ntail = S.L - S.Lq;
   const int tl = lane >> 1, half = lane & 1;
@@ -122,7 +124,7 @@ __device__ __forceinline__ void tail_pass(const DecodeArgs& a, const DecodeSeq& 
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
     sig[g] += dpp_mov<kQuadXor1>(0.f, sig[g]);
-    if (idx >= ntail) sig[g] = -__builtin_inff();
+    if (idx >= ntail || S.Lq + idx >= lim[g]) sig[g] = -__builtin_inff();
   }
   softmax_pass<GQ>(st, sig, half, tl, p_lds);
   wave_lds_sync();
@@ -144,9 +146,9 @@ __device__ __forceinline__ void tail_pass(const DecodeArgs& a, const DecodeSeq& 
   wave_lds_sync();
 }
 
-// Locate this workgroup's (sequence, kv head, split).
+// Locate this workgroup's (sequence, kv head, row group, split).
 struct Work {
-  int si, h, sp;
+  int si, h, rg, sp;
 };
 
 __device__ __forceinline__ Work find_work(const DecodeArgs& a) {
@@ -154,7 +156,41 @@ __device__ __forceinline__ Work find_work(const DecodeArgs& a) {
   int si = 0;
   for (int i = 1; i < a.nseq; ++i) si = (a.seq[i].wg_begin <= wg) ? i : si;
   const int local = wg - a.seq[si].wg_begin;
-  return {si, local / a.seq[si].nsplit, local % a.seq[si].nsplit};
+  const int hv = local / a.seq[si].nsplit;
+  return {si, hv / a.nrg, hv % a.nrg, local % a.seq[si].nsplit};
+}
+
+// Row g of the workgroup's row group: chunk query j, query head hd.
+struct QueryRow {
+  int j, hd;
+};
+
+__device__ __forceinline__ QueryRow query_row(const DecodeArgs& a, int h, int rg, int g) {
+  const int x = g / a.gqh;
+  return {rg * a.qpr + x, h * a.gqh + (g - x * a.gqh)};
+}
+
+// Query row g in q / out ([batch][nqry][Hq]).
+__device__ __forceinline__ size_t q_index(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int g) {
+  const QueryRow r = query_row(a, h, rg, g);
+  return ((size_t)S.seq * a.nqry + r.j) * a.hq + r.hd;
+}
+
+// Tokens [0, limit) are visible to row g.
+__device__ __forceinline__ int row_limit(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int g) {
+  return S.L - a.nqry + 1 + query_row(a, h, rg, g).j;
+}
+
+// The smallest limit of the row group: every token below it is visible to
+// every row.
+__device__ __forceinline__ int group_limit(const DecodeArgs& a, const DecodeSeq& S, int rg) {
+  return S.L - a.nqry + 1 + rg * a.qpr;
+}
+
+template <int GQ>
+__device__ __forceinline__ void row_limits(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int (&lim)[GQ]) {
+#pragma unroll
+  for (int g = 0; g < GQ; ++g) lim[g] = row_limit(a, S, h, rg, g);
 }
 
 // Per-wave partial results of GQ query heads, staged for the combine.
@@ -192,7 +228,7 @@ __device__ __forceinline__ void stage_state(State<GQ>& st, Reduce<GQ>& r, int la
 // After a barrier: merge the waves' partial results and write the record of
 // split sp for the GQ query heads of kv head h.
 template <int GQ>
-__device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSeq& S, int h, int sp,
+__device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int sp,
                                              const Reduce<GQ>& r) {
   for (int idx = threadIdx.x; idx < GQ * kHeadDim; idx += blockDim.x) {
     const int g = idx / kHeadDim, c = idx % kHeadDim;
@@ -202,11 +238,13 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSe
     float val = 0.f, lsum = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      const float f = __builtin_amdgcn_exp2f(r.m[w][g] - M);
+      // a wave that saw no visible token of the row has m = -inf, l = 0
+      const float f = r.m[w][g] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(r.m[w][g] - M);
       val = fmaf(f, r.acc[w][idx], val);
       lsum = fmaf(f, r.l[w][g], lsum);
     }
-    float* rec = a.ws + ((size_t)(S.ws_base + sp) * a.hq + (size_t)h * GQ + g) * kRecFloats;
+    const QueryRow qr = query_row(a, h, rg, g);
+    float* rec = a.ws + ((size_t)(S.ws_base + sp) * a.hq * a.nqry + (size_t)qr.j * a.hq + qr.hd) * kRecFloats;
     rec[4 + c] = val;
     if (c == 0) { rec[0] = M; rec[1] = lsum; }
   }
@@ -214,9 +252,9 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSe
 
 // The fp16 tail split: every wave takes passes of 32 tokens.
 template <int GQ>
-__device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq& S, int h, const uint8_t* blk,
-                                           const float (&qs0)[GQ], const float (&qs1)[GQ], float* qp,
-                                           float* pl, State<GQ>& st, int lane, int wv) {
+__device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq& S, int h, int rg,
+                                           const uint8_t* blk, const float (&qs0)[GQ], const float (&qs1)[GQ],
+                                           float* qp, float* pl, State<GQ>& st, int lane, int wv) {
   constexpr int QS = QStride<GQ>::value;
   // Fused append: this workgroup alone reads the ring of (sequence, head h)
   // in this launch; it first stores the tokens appended by the call, which
@@ -242,7 +280,9 @@ __device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq&
     qp[(2 * lane + 1) * QS + g] = qs1[g];
   }
   wave_lds_sync();
-  for (int pass = wv; pass * 32 < S.L - S.Lq; pass += kWaves) tail_pass<GQ>(a, S, blk, pass, qp, pl, st, lane);
+  int lim[GQ];
+  row_limits<GQ>(a, S, h, rg, lim);
+  for (int pass = wv; pass * 32 < S.L - S.Lq; pass += kWaves) tail_pass<GQ>(a, S, blk, pass, qp, pl, st, lim, lane);
 }
 
 template <int GQ>
@@ -259,12 +299,11 @@ __device__ __forceinline__ void init_state(State<GQ>& st) {
 // This lane's two channels (2*lane, 2*lane+1) of the GQ query heads,
 // pre-scaled to base 2.
 template <int GQ>
-__device__ __forceinline__ void load_q_scaled(const DecodeArgs& a, const DecodeSeq& S, int h, int lane,
+__device__ __forceinline__ void load_q_scaled(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int lane,
                                               float (&qs0)[GQ], float (&qs1)[GQ]) {
-  const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)h * GQ) * kHeadDim;
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(qrow + g * kHeadDim)[lane];
+    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + q_index(a, S, h, rg, g) * kHeadDim)[lane];
     qs0[g] = h2f(w & 0xFFFF) * a.qscale;
     qs1[g] = h2f(w >> 16) * a.qscale;
   }

@@ -285,7 +285,9 @@ struct MatrixStages {
   static constexpr int value = (MatrixOcc<BK, BV, BPG, GQ>::value >= 4 || GQ > 4 || BK + BV >= 16) ? 2 : 3;
 };
 
-template <int BK, int BV, int BPG, int GQ>
+// CAUSAL: chunk queries (rows see tokens below their own limit); the
+// single-token decode instantiations carry no masking code.
+template <int BK, int BV, int BPG, int GQ, bool CAUSAL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MatrixOcc<BK, BV, BPG, GQ>::value))) void
 decode_mfma_kernel(DecodeArgs a) {
   constexpr int NH = MatrixHeads<GQ>::value;  // heads in the score rows
@@ -327,15 +329,15 @@ decode_mfma_kernel(DecodeArgs a) {
 
   if (wk.sp >= S.nq) {  // fp16 tail tokens: vector path
     float qs0[GQ], qs1[GQ];
-    load_q_scaled<GQ>(a, S, wk.h, lane, qs0, qs1);
+    load_q_scaled<GQ>(a, S, wk.h, wk.rg, lane, qs0, qs1);
     State<GQ> st;
     init_state<GQ>(st);
     static_assert(kHeadDim * QStride<GQ>::value <= (3 * NH + kDzRows) * kQRow, "tail query fits the Q' area");
     static_assert(32 * GQ <= kPRow * NH, "tail weights fit the weight area");
-    tail_split<GQ>(a, S, wk.h, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st, lane, wv);
+    tail_split<GQ>(a, S, wk.h, wk.rg, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st, lane, wv);
     stage_state<GQ>(st, red, lane, wv);
     __syncthreads();
-    write_record<GQ>(a, S, wk.h, wk.sp, red);
+    write_record<GQ>(a, S, wk.h, wk.rg, wk.sp, red);
     return;
   }
 
@@ -344,7 +346,6 @@ decode_mfma_kernel(DecodeArgs a) {
   const int col = lane & 15, row = lane >> 4;     // MFMA column, lane row
   const int hc = col >> 2, xc = col & 3, part = col & 1, hs = col / RS;
   const int ng = kHeadDim / a.gv, gsel = xc & (ng - 1);
-  const uint16_t* qrow = a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * GQ) * kHeadDim;
   const __amdgpu_buffer_rsrc_t rs = head_rsrc(blk, a.head_stride);
   LaneOffsets lo;
   lo.km = 4 * lane;
@@ -406,7 +407,7 @@ decode_mfma_kernel(DecodeArgs a) {
   }
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(qrow + g * kHeadDim)[lane];
+    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + q_index(a, S, wk.h, wk.rg, g) * kHeadDim)[lane];
     const float q0 = h2f(w & 0xFFFF), q1 = h2f(w >> 16);
     const float mx = wave_max(fmaxf(fabsf(q0), fabsf(q1)));
     int e = 0;
@@ -423,6 +424,16 @@ decode_mfma_kernel(DecodeArgs a) {
   float cs[HPL];
 #pragma unroll
   for (int hh = 0; hh < HPL; ++hh) cs[hh] = pickn<NH>(csc, HPL * row + hh);
+  // Chunk queries: row g sees tokens below lim[g]; blocks that reach glim
+  // (the row group's smallest limit) mask their later tokens per row.
+  // Single-token decode: glim = L, past every packed block.
+  const int glim = group_limit(a, S, wk.rg);
+  int lim[HPL];
+#pragma unroll
+  for (int hh = 0; hh < HPL; ++hh) {
+    const int g = HPL * row + hh;
+    lim[hh] = g < GQ ? row_limit(a, S, wk.h, wk.rg, g) : S.L;
+  }
 
   // Zero-point terms sum_c z[c] q~[c] of 16 key groups and the NH heads, in
   // one MFMA chain (A = z of group col, B = q~ of head col / RS), scaled like
@@ -522,6 +533,15 @@ decode_mfma_kernel(DecodeArgs a) {
     for (int hh = 0; hh < HPL; ++hh)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) raw[hh][mb] = d[mb][2 * hh] + d[mb][2 * hh + 1];  // hi + lo rows
+    const int tok = (j0 + kWaves * (i / BPG)) * a.gk + (i % BPG) * 32;
+    const bool masked = CAUSAL && tok + 32 > glim;
+    if (masked) {
+#pragma unroll
+      for (int hh = 0; hh < HPL; ++hh)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+          if (tok + 16 * mb + col >= lim[hh]) raw[hh][mb] = -__builtin_inff();
+    }
 
     // online softmax (base 2) per head over these 32 tokens; cs > 0, so the
     // maximum is taken before scaling.  The reference m moves only when a
@@ -551,7 +571,8 @@ decode_mfma_kernel(DecodeArgs a) {
         b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
         b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
         const float mnew = b > m[hh] ? b + kLazyMargin : m[hh];
-        alpha[hh] = __builtin_amdgcn_exp2f(m[hh] - mnew);  // 1 where the reference stays
+        // 1 where the reference stays (also a row with no visible token yet)
+        alpha[hh] = mnew == m[hh] ? 1.f : __builtin_amdgcn_exp2f(m[hh] - mnew);
         l[hh] *= alpha[hh];
         m[hh] = mnew;
       }
@@ -579,6 +600,10 @@ decode_mfma_kernel(DecodeArgs a) {
     for (int hh = 0; hh < HPL; ++hh) {
       e[hh][0] = __builtin_amdgcn_exp2f(fmaf(raw[hh][0], cs[hh], -m[hh]));
       e[hh][1] = __builtin_amdgcn_exp2f(fmaf(raw[hh][1], cs[hh], -m[hh]));
+      if (masked) {  // masked tokens weigh 0, also while m is still -inf
+        e[hh][0] = raw[hh][0] == -__builtin_inff() ? 0.f : e[hh][0];
+        e[hh][1] = raw[hh][1] == -__builtin_inff() ? 0.f : e[hh][1];
+      }
       l[hh] += e[hh][0] + e[hh][1];
     }
     wave_lds_sync();
@@ -717,13 +742,17 @@ decode_mfma_kernel(DecodeArgs a) {
     }
   }
   __syncthreads();
-  write_record<GQ>(a, S, wk.h, wk.sp, red);
+  write_record<GQ>(a, S, wk.h, wk.rg, wk.sp, red);
 }
 
 template <int BK, int BV, int BPG, int GQ>
 int launch_t(const DecodeArgs& a, void* stream) {
-  hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG, GQ>), dim3(a.total_wg), dim3(64 * kWaves), 0,
-                     (hipStream_t)stream, a);
+  if (a.nqry > 1)
+    hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG, GQ, true>), dim3(a.total_wg), dim3(64 * kWaves), 0,
+                       (hipStream_t)stream, a);
+  else
+    hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG, GQ, false>), dim3(a.total_wg), dim3(64 * kWaves), 0,
+                       (hipStream_t)stream, a);
   return (int)hipGetLastError();
 }
 

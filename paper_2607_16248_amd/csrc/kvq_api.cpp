@@ -123,16 +123,16 @@ HeadLayout layout_of(const kvq_cache_desc* d, int bk, int bv) {
 // Split length of one launch's sequences (one bit class): the launch fills
 // one round of the resident workgroups of its kernel.  Classes launch one
 // after another, so each gets the whole device.
-int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs) {
+int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int nrg, int occ_rows) {
   const int gk = c->d.key_group;
   if (c->split_tokens > 0) return c->split_tokens;
   int64_t total = 0, lq_max = 0, tails = 0;
   int occ = 4;
   for (int i : seqs) {
-    total += (int64_t)c->Lq[i] * c->d.num_kv_heads;
+    total += (int64_t)c->Lq[i] * c->d.num_kv_heads * nrg;
     lq_max = std::max<int64_t>(lq_max, c->Lq[i]);
-    if (c->L[i] > c->Lq[i]) tails += c->d.num_kv_heads;
-    occ = std::min(occ, c->occupancy[i]);
+    if (c->L[i] > c->Lq[i]) tails += (int64_t)c->d.num_kv_heads * nrg;
+    occ = std::min(occ, occ_rows > 0 && c->matrix[i] ? occ_rows : c->occupancy[i]);
   }
   // The fp16-tail workgroups (one per sequence and kv head with tail tokens)
   // share the same round of resident workgroups: a workgroup that has to
@@ -319,19 +319,58 @@ size_t kvq_workspace_bytes(const kvq_cache* c) {
 
 namespace {
 
+// Query rows of a launch (see DecodeArgs): nqry queries per sequence in row
+// groups of qpr queries, rows = qpr * (Hq / Hkv) rows per workgroup.
+struct Rows {
+  int nqry = 1, qpr = 1, nrg = 1, rows = 1;
+};
+
+// Single-token decode: one row group of the kv head's query heads.  Chunk
+// queries: the largest row group a kernel has (matrix: 4, 5, 8 rows; vector:
+// also 1, 2) made of whole queries, with a whole number of groups.
+Rows rows_for(const kvq_cache* c, bool matrix, int nqry) {
+  const int gqh = c->d.num_q_heads / c->d.num_kv_heads;
+  Rows r;
+  r.rows = gqh;
+  if (nqry <= 1) return r;
+  static const int kMatrixRows[] = {8, 5, 4}, kVectorRows[] = {8, 5, 4, 2, 1};
+  const int* cand = matrix ? kMatrixRows : kVectorRows;
+  const int ncand = matrix ? 3 : 5;
+  r.nqry = nqry;
+  for (int k = 0; k < ncand; ++k) {
+    const int rg = cand[k];
+    if (rg % gqh == 0 && nqry % (rg / gqh) == 0) {
+      r.qpr = rg / gqh;
+      r.nrg = nqry / r.qpr;
+      r.rows = rg;
+      return r;
+    }
+  }
+  r.qpr = 1;  // not reached: rg = gqh always qualifies
+  r.nrg = nqry;
+  return r;
+}
+
 struct SplitPlan {
   std::vector<int32_t> st, nq, ns, base;  // per sequence: split length, packed splits, all splits, first record
   int64_t records = 0;
+  int nqry = 1;
 };
 
-SplitPlan plan_splits(const kvq_cache* c) {
+SplitPlan plan_splits(const kvq_cache* c, int nqry = 1) {
   SplitPlan p;
+  p.nqry = nqry;
   const int B = c->d.batch;
   p.st.assign(B, 0);
   std::map<std::pair<int, int>, std::vector<int>> classes;
   for (int i = 0; i < B; ++i) classes[{c->bk[i], c->bv[i]}].push_back(i);
   for (auto& cl : classes) {
-    const int32_t st = split_tokens_for(c, cl.second);
+    const bool matrix = c->matrix[cl.second[0]] != 0;
+    const Rows r = rows_for(c, matrix, nqry);
+    const int occ = nqry > 1 && matrix
+                        ? kvq::matrix_decode_occupancy(cl.first.first, cl.first.second, c->d.key_group, r.rows)
+                        : 0;
+    const int32_t st = split_tokens_for(c, cl.second, r.nrg, occ);
     for (int i : cl.second) p.st[i] = st;
   }
   p.nq.resize(B);
@@ -359,7 +398,7 @@ struct FusedAppend {
 kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, void* ws, size_t ws_bytes,
                         void* stream, const FusedAppend* app = nullptr) {
   const kvq_cache_desc& d = c->d;
-  const size_t need = (size_t)p.records * d.num_q_heads * kvq::kRecFloats * sizeof(float);
+  const size_t need = (size_t)p.records * d.num_q_heads * p.nqry * kvq::kRecFloats * sizeof(float);
   if (!q) return fail(KVQ_ERR_ARG, "q must be a device pointer");
   if (need > 0 && !ws) return fail(KVQ_ERR_ARG, "workspace is NULL");
   if (ws_bytes < need) return fail(KVQ_ERR_CAPACITY, "workspace holds %zu bytes, this call needs %zu", ws_bytes, need);
@@ -380,6 +419,8 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.hq = d.num_q_heads; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
     a.split_tokens = p.st[cls.second[0]];
     a.qscale = qscale;
+    const Rows r = rows_for(c, c->matrix[cls.second[0]] != 0, p.nqry);
+    a.nqry = r.nqry; a.qpr = r.qpr; a.nrg = r.nrg; a.gqh = d.num_q_heads / d.num_kv_heads;
     if (app) {
       a.K_new = static_cast<const uint16_t*>(app->K);
       a.V_new = static_cast<const uint16_t*>(app->V);
@@ -393,13 +434,13 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
       s.L_old = app ? (*app->L_old)[i] : c->L[i];
       s.nq = p.nq[i]; s.nsplit = p.ns[i]; s.ws_base = p.base[i];
       s.wg_begin = wg;
-      wg += p.ns[i] * d.num_kv_heads;
+      wg += p.ns[i] * d.num_kv_heads * r.nrg;
     }
     a.nseq = n;
     a.total_wg = wg;
     const int e = c->matrix[cls.second[0]]
-                      ? kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, d.num_q_heads / d.num_kv_heads, stream)
-                      : kvq::launch_decode(a, cls.first.first, cls.first.second, d.num_q_heads / d.num_kv_heads, stream);
+                      ? kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, r.rows, stream)
+                      : kvq::launch_decode(a, cls.first.first, cls.first.second, r.rows, stream);
     if (e) return hip_fail(e, "decode launch");
   }
   return KVQ_OK;
@@ -413,7 +454,7 @@ kvq_status run_merge(const kvq_cache* c, const SplitPlan& p, const void* ws, flo
     kvq::MergeArgs m{};
     m.ws = static_cast<const float*>(ws);
     m.out = out;
-    m.hq = d.num_q_heads;
+    m.hq = d.num_q_heads * p.nqry;  // out [batch][nqry][Hq] = [batch][nqry * Hq]
     int n = 0;
     for (int i = b; i < std::min(d.batch, b + kvq::kMaxSeqPerLaunch); ++i) {
       m.seq[n].seq = i; m.seq[n].nsplit = p.ns[i]; m.seq[n].ws_base = p.base[i];
@@ -503,6 +544,27 @@ kvq_status kvq_decode_merge(const kvq_cache* c, const void* ws, float* out, void
   if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
   const kvq_status st = run_merge(c, plan_splits(c), ws, out, stream);
   return st == KVQ_OK ? ok() : st;
+}
+
+size_t kvq_chunk_workspace_bytes(const kvq_cache* c, int32_t n_q) {
+  if (!c || n_q < 1 || n_q > KVQ_MAX_CHUNK) return 0;
+  return kvq_workspace_bytes(c) * (size_t)n_q;
+}
+
+kvq_status kvq_chunk_attention(const kvq_cache* c, const void* q, int32_t n_q, float* out, void* ws,
+                               size_t ws_bytes, void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (n_q < 1 || n_q > KVQ_MAX_CHUNK) return fail(KVQ_ERR_ARG, "n_q = %d outside [1, %d]", n_q, KVQ_MAX_CHUNK);
+  if (!q || !out) return fail(KVQ_ERR_ARG, "q and out must be device pointers");
+  for (int i = 0; i < c->d.batch; ++i)
+    if (c->L[i] < n_q)
+      return fail(KVQ_ERR_ARG, "sequence %d holds %d tokens, fewer than the %d chunk queries", i, c->L[i], n_q);
+  const SplitPlan p = plan_splits(c, n_q);
+  kvq_status st = run_partials(c, p, q, ws, ws_bytes, stream);
+  if (st != KVQ_OK) return st;
+  st = run_merge(c, p, ws, out, stream);
+  if (st != KVQ_OK) return st;
+  return ok();
 }
 
 kvq_status kvq_dequant(const kvq_cache* c, int32_t seq, int32_t tok0, int32_t ntok, float* K_out, float* V_out,

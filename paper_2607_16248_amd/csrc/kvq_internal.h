@@ -84,10 +84,17 @@ struct DecodeSeq {
   int32_t L_old;      // tokens [L_old, L) arrive in this call (fused append), else L_old = L
 };
 
+// Query rows.  A launch attends nqry queries per sequence: query j is the
+// token at position L - nqry + j and sees tokens [0, L - nqry + 1 + j)
+// (nqry = 1: single-token decode over the whole cache).  The rows of one kv
+// head h are (query j, head h*gqh + x); a workgroup takes a row group of qpr
+// consecutive queries times the gqh heads (GQ = qpr*gqh rows, the kernel's
+// template size), row group rg of nrg = nqry / qpr.  q and out are
+// [batch][nqry][Hq][128]; a split record row is j*Hq + head.
 struct DecodeArgs {
   const uint8_t* arena;
-  const uint16_t* q;  // fp16 [batch][Hq][128]
-  float* ws;          // split records [.][Hq][kRecFloats]
+  const uint16_t* q;  // fp16 [batch][nqry][Hq][128]
+  float* ws;          // split records [.][nqry * Hq][kRecFloats]
   // fused append: fp16 [batch][n_max][Hkv][128] rows of the tokens [L_old, L),
   // written into the ring by the fp16 tail split of their (sequence, head)
   // before it attends over them; null when the call appends nothing
@@ -97,6 +104,7 @@ struct DecodeArgs {
   uint64_t head_stride;
   uint32_t kc, km, vc, vm, tk, tv;
   int32_t hq, hkv, gk, gv, W, split_tokens, nseq, total_wg;
+  int32_t nqry, qpr, nrg, gqh;
   float qscale;       // log2(e) / sqrt(d)
   DecodeSeq seq[kMaxSeqPerLaunch];
 };
@@ -107,8 +115,8 @@ struct MergeSeq {
 
 struct MergeArgs {
   const float* ws;
-  float* out;         // fp32 [batch][Hq][128]
-  int32_t hq, nseq;
+  float* out;         // fp32 [batch][hq][128]
+  int32_t hq, nseq;   // hq: record rows per split (query heads times queries)
   MergeSeq seq[kMaxSeqPerLaunch];
 };
 

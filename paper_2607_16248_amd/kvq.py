@@ -20,7 +20,7 @@ STATUS_NAMES = ["KVQ_OK", "KVQ_ERR_ARG", "KVQ_ERR_UNSUPPORTED", "KVQ_ERR_CAPACIT
 
 EXPORTED = ["kvq_cache_bytes", "kvq_cache_init", "kvq_cache_destroy", "kvq_cache_reset",
             "kvq_seq_len", "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention", "kvq_append_decode",
-            "kvq_decode_partials", "kvq_decode_merge",
+            "kvq_decode_partials", "kvq_decode_merge", "kvq_chunk_workspace_bytes", "kvq_chunk_attention",
             "kvq_dequant", "kvq_export_bytes", "kvq_export", "kvq_check",
             "kvq_set_split_tokens", "kvq_last_error", "kvq_version",
             "dgap_workspace_bytes", "dgap_info_floats", "dgap_restore"]
@@ -73,6 +73,8 @@ def lib():
         "kvq_append": ([P, P, P, I32, ctypes.POINTER(I32), P], ctypes.c_int),
         "kvq_workspace_bytes": ([P], S),
         "kvq_decode_attention": ([P, P, P, P, S, P], ctypes.c_int),
+        "kvq_chunk_workspace_bytes": ([P, ctypes.c_int32], S),
+        "kvq_chunk_attention": ([P, P, ctypes.c_int32, P, P, S, P], ctypes.c_int),
         "kvq_append_decode": ([P, P, P, I32, ctypes.POINTER(I32), P, P, P, S, P], ctypes.c_int),
         "kvq_decode_partials": ([P, P, P, S, P], ctypes.c_int),
         "kvq_decode_merge": ([P, P, P, P], ctypes.c_int),
@@ -177,6 +179,19 @@ def kvq_decode_attention(cache: int, q, out, ws, ws_bytes: Optional[int] = None,
     _check(lib().kvq_decode_attention(cache, _ptr(q), _ptr(out), _ptr(ws), int(ws_bytes), _stream(stream)))
 
 
+def kvq_chunk_workspace_bytes(cache: int, n_q: int) -> int:
+    return int(lib().kvq_chunk_workspace_bytes(cache, int(n_q)))
+
+
+def kvq_chunk_attention(cache: int, q, n_q: int, out, ws, ws_bytes: Optional[int] = None, stream=None) -> None:
+    """The last n_q tokens of every sequence attend causally: q fp16 [batch][n_q][Hq][d],
+    out fp32 [batch][n_q][Hq][d]."""
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(lib().kvq_chunk_attention(cache, _ptr(q), int(n_q), _ptr(out), _ptr(ws), int(ws_bytes),
+                                     _stream(stream)))
+
+
 def kvq_append_decode(cache: int, K, V, n_new: Sequence[int], q, out, ws, ws_bytes: Optional[int] = None,
                       n_max: Optional[int] = None, stream=None) -> None:
     """kvq_append then kvq_decode_attention in one call (two launches when no key group fills)."""
@@ -279,6 +294,18 @@ class KVCache:
             out = torch.empty((self.batch, self.num_q_heads, self.head_dim), dtype=torch.float32,
                               device=q.device)
         kvq_decode_attention(self.handle, q, out, self.workspace(), stream=stream)
+        return out
+
+    def chunk(self, q, out=None, stream=None):
+        """Causal attention of the last q.shape[1] tokens of every sequence."""
+        import torch
+        n_q = int(q.shape[1])
+        if out is None:
+            out = torch.empty((self.batch, n_q, self.num_q_heads, self.head_dim), dtype=torch.float32,
+                              device=q.device)
+        need = kvq_chunk_workspace_bytes(self.handle, n_q)
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=self.arena.device)
+        kvq_chunk_attention(self.handle, q, n_q, out, ws, stream=stream)
         return out
 
     def append_decode(self, K, V, q, n_new=None, out=None, stream=None):

@@ -190,6 +190,29 @@ def test_split_setting_and_workspace_bound():
         kvq.kvq_cache_destroy(h)
 
 
+def test_chunk_attention_sizes_and_argument_errors():
+    """Every check of kvq_chunk_attention precedes any launch."""
+    d = desc(max_tokens=4096, bits_k=[1], bits_v=[1])
+    h = kvq.kvq_cache_init(d, FAKE_ARENA, kvq.kvq_cache_bytes(d))
+    F = FAKE_ARENA
+    try:
+        one = kvq.kvq_workspace_bytes(h)
+        assert kvq.kvq_chunk_workspace_bytes(h, 1) == one
+        assert kvq.kvq_chunk_workspace_bytes(h, 16) == 16 * one
+        assert kvq.kvq_chunk_workspace_bytes(h, 1024) == 1024 * one
+        assert kvq.kvq_chunk_workspace_bytes(h, 0) == 0 and kvq.kvq_chunk_workspace_bytes(h, 1025) == 0
+        for n_q, q, out in [(0, F, F), (1025, F, F), (1, None, F), (1, F, None)]:
+            with pytest.raises(kvq.KvqError) as e:
+                kvq.kvq_chunk_attention(h, q, n_q, out, F, ws_bytes=1 << 30)
+            assert e.value.status == kvq.ERR_ARG, (n_q, q, out)
+        # an empty sequence holds fewer tokens than any chunk
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.kvq_chunk_attention(h, F, 1, F, F, ws_bytes=1 << 30)
+        assert e.value.status == kvq.ERR_ARG and "fewer than" in kvq.kvq_last_error()
+    finally:
+        kvq.kvq_cache_destroy(h)
+
+
 def test_dgap_sizes_and_argument_errors():
     """dgap_restore checks every argument before it launches anything."""
     # workspace: chunk statistics (256-byte aligned) + one 8-byte key per window slot per chunk

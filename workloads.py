@@ -16,7 +16,7 @@ tensor, *extra])`` so any single (layer, seq, kv head) unit can be rebuilt on
 its own, on the host, without generating the rest of the workload.
 
 Tensor ids: 0 = q, 1 = K, 2 = V, 3 = outlier channel choice, 4 = context
-lengths, 5 = appended K, 6 = appended V.
+lengths, 5 = appended K, 6 = appended V, 7 = chunk queries (with n_q).
 """
 from __future__ import annotations
 
@@ -27,7 +27,7 @@ import numpy as np
 
 MAGIC = 0x4B5651  # "KVQ"
 
-T_Q, T_K, T_V, T_OUTLIER, T_LENS, T_APPEND_K, T_APPEND_V = range(7)
+T_Q, T_K, T_V, T_OUTLIER, T_LENS, T_APPEND_K, T_APPEND_V, T_Q_CHUNK = range(8)
 
 # Inputs are kept at |x| <= this bound so that a 1-bit group's range
 # (max - min) can never exceed the largest finite fp16 scale; only the
@@ -127,6 +127,12 @@ def gen_q(w: Workload, layer: int = 0, seq: int = 0) -> np.ndarray:
     """q for one sequence: fp16 [Hq][d], ~N(0,1)."""
     r = _rng(w.cfg_id, layer, seq, T_Q)
     return r.standard_normal((w.num_q_heads, w.head_dim), dtype=np.float32).astype(np.float16)
+
+
+def gen_q_chunk(w: Workload, n_q: int, layer: int = 0, seq: int = 0) -> np.ndarray:
+    """Queries of the last n_q positions of one sequence: fp16 [n_q][Hq][d], ~N(0,1)."""
+    r = _rng(w.cfg_id, layer, seq, T_Q_CHUNK, n_q)
+    return r.standard_normal((n_q, w.num_q_heads, w.head_dim), dtype=np.float32).astype(np.float16)
 
 
 def gen_kv(w: Workload, layer: int, seq: int, n: Optional[int] = None,
