@@ -12,7 +12,9 @@ Prints ONE JSON line.  value = packed-KV bytes the decode kernels must read
 per step (codes + fp16 scales/zeros + fp16 tail, all layers) / step time.
 The line also carries "dgap": DGAP's logit-side step (features, detector,
 top-K window, corrector, merge) on one logit row of the workload's model
-vocabulary, timed on its own (--no-dgap skips it).
+vocabulary, timed on its own (--no-dgap skips it), and "chunk": the last
+4 / 16 / 64 tokens attending causally over the same caches
+(kvq_chunk_attention; --no-chunk skips it).
 """
 from __future__ import annotations
 
@@ -161,6 +163,53 @@ def dgap_leg(workload_idx: int, bits: int, iters: int):
     return out
 
 
+CHUNK_SIZES = (4, 16, 64)
+
+
+def chunk_leg(handles, w, launch_bytes: int, stream, iters: int):
+    """Chunk queries over the same layer caches: the last n_q tokens of the
+    sequence attend causally (chunked prefill, speculative verification),
+    timed with HIP events on the launch stream over the rotating layers."""
+    import torch
+
+    from paper_2607_16248_amd import kvq
+
+    dev = torch.device("cuda:0")
+    layers = len(handles)
+    out = {"n_q": list(CHUNK_SIZES), "us_per_layer": [], "query_tokens_per_s_per_layer": [],
+           "cache_gbs_one_pass": [], "useful_tflops": [], "row_groups_per_kv_head": []}
+    L = min(kvq.kvq_seq_len(handles[0], s) for s in range(w.batch))
+    for n_q in CHUNK_SIZES:
+        g = torch.Generator(device=dev).manual_seed(n_q)
+        q = torch.randn((w.batch, n_q, w.num_q_heads, w.head_dim), generator=g, device=dev).half()
+        o = torch.empty((w.batch, n_q, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+        need = max(kvq.kvq_chunk_workspace_bytes(h, n_q) for h in handles)
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+        for i in range(8):
+            kvq.kvq_chunk_attention(handles[i % layers], q, n_q, o, ws, need, stream=stream)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(iters):
+            kvq.kvq_chunk_attention(handles[i % layers], q, n_q, o, ws, need, stream=stream)
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / iters
+        # QK and PV: 2 * 2 * d flops per (query, head, visible token)
+        flops = 4 * w.head_dim * w.num_q_heads * w.batch * sum(L - n_q + 1 + i for i in range(n_q))
+        gq = w.group_q
+        rows = 8 if (gq == 4 and n_q % 2 == 0) or gq == 8 else gq
+        out["us_per_layer"].append(round(us, 3))
+        out["query_tokens_per_s_per_layer"].append(round(n_q * w.batch / (us * 1e-6), 1))
+        out["cache_gbs_one_pass"].append(round(launch_bytes / (us * 1e-6) / 1e9, 2))
+        out["useful_tflops"].append(round(flops / (us * 1e-6) / 1e12, 2))
+        out["row_groups_per_kv_head"].append(n_q * gq // rows)
+        del q, o, ws
+    out["note"] = ("each row group of up to 8 (query, head) rows is one pass over the kv head's cache; "
+                   "the useful flops count each visible (query, head, token) once")
+    return out
+
+
 def dgap_cpu_baseline(workload_idx: int, bits: int) -> float:
     """Part of the CPU-baseline leg: the DGAP oracle (fp64, one thread) on the
     same row, microseconds per corrected step."""
@@ -188,6 +237,7 @@ def main():
     ap.add_argument("--cpu-heads", type=int, default=4, help="kv heads in the CPU-baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dgap", action="store_true", help="skip the DGAP logit-side leg")
+    ap.add_argument("--no-chunk", action="store_true", help="skip the chunk-query leg")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="end with 4 plain device copies of 256 MiB (counter calibration)")
     args = ap.parse_args()
@@ -428,7 +478,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.key_group // 32},{w.group_q}>" if matrix_path(w) else
+            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.key_group // 32},{w.group_q},false>" if matrix_path(w) else
                        f"decode_split_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.group_q}>"),
             "bytes_per_launch": launch_bytes,
             "kernel_source_sha256_16": source_digest(),
@@ -441,6 +491,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if not args.no_chunk:
+        log("[bench] chunk queries")
+        result["chunk"] = chunk_leg(handles, w, launch_bytes, stream, max(2 * layers, 32))
     if not args.no_dgap:
         log("[bench] DGAP logit-side step")
         result["dgap"] = dgap_leg(args.workload, w.bits_k[0], 200)
