@@ -67,6 +67,16 @@ typedef struct {
   int32_t fp16_window;    /* recent tokens kept in fp16, >= 0 */
   const uint8_t* bits_k;  /* host array [batch] of key bits, each 1, 2, 4 or 8 */
   const uint8_t* bits_v;  /* host array [batch] of value bits, each 1, 2, 4 or 8 */
+  /* Paged layout (serving): 0 = one contiguous region per sequence.  Else
+   * the packed codes and scales of every page_tokens consecutive tokens of
+   * a sequence (all kv heads) live in one page of a pool shared by the
+   * batch, found through a block table; pages are taken as sequences grow
+   * and returned by kvq_seq_release.  A power of two >= key_group; every
+   * sequence must then use the same bit widths. */
+  int32_t page_tokens;
+  /* Pages in the pool (paged layout only); 0 = enough for every sequence
+   * at max_tokens.  Fewer pages let the batch share a smaller pool. */
+  int32_t num_pages;
 } kvq_cache_desc;
 
 /* Opaque host-side handle.  It owns no device memory. */
@@ -93,12 +103,23 @@ kvq_status kvq_cache_reset(kvq_cache* cache, void* stream);
 /* Current length L of a sequence (host bookkeeping), or -1 if out of range. */
 int64_t kvq_seq_len(const kvq_cache* cache, int32_t seq);
 
+/* Empty one sequence (host bookkeeping only, no launch): its length
+ * becomes 0 and, in a paged cache, its pages return to the pool, so the
+ * slot can take a new sequence while the others keep decoding. */
+kvq_status kvq_seq_release(kvq_cache* cache, int32_t seq);
+
+/* Free pages in the pool of a paged cache; -1 for a contiguous cache or
+ * a NULL handle. */
+int64_t kvq_free_pages(const kvq_cache* cache);
+
 /* Append tokens and quantize every key group that leaves the fp16 window
  * (the fused quantize-on-append step).
  *   K, V : device fp16 [batch][n_max][Hkv][d]; sequence i appends rows
  *          0 .. n_new[i]-1 of its slice.  Read only.
  *   n_new: host int32 [batch], 0 <= n_new[i] <= n_max.
- * KVQ_ERR_CAPACITY if any L + n_new exceeds max_tokens (nothing appended).
+ * KVQ_ERR_CAPACITY if any L + n_new exceeds max_tokens, or if a paged
+ * cache's pool has too few free pages for the new packed tokens (nothing
+ * appended).
  * Inputs must be finite fp16 whose group range fits the fp16 scale
  * (|x| <= 32752 always does); a violation is reported later by kvq_check.
  * Prefill is an append with n_new = prompt length. */

@@ -8,6 +8,7 @@ from .kvq import (KVCache, KvqError, kvq_append, kvq_append_decode, kvq_cache_by
                   kvq_cache_init, kvq_cache_reset, kvq_check, kvq_chunk_attention, kvq_chunk_workspace_bytes,
                   kvq_decode_attention,
                   kvq_decode_merge, kvq_decode_partials, kvq_dequant,
-                  kvq_export, kvq_export_bytes, kvq_last_error, kvq_seq_len, kvq_set_split_tokens,
+                  kvq_export, kvq_export_bytes, kvq_free_pages, kvq_last_error, kvq_seq_len, kvq_seq_release,
+                  kvq_set_split_tokens,
                   kvq_version, kvq_workspace_bytes, make_desc)
 from .kvq import dgap_info_floats, dgap_params, dgap_restore, dgap_workspace_bytes  # noqa: F401

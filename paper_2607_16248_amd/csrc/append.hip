@@ -93,9 +93,14 @@ __device__ __forceinline__ void pack_value_blocks_matrix(const uint8_t* codes, i
 
 __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, int gi, int bk,
                                int bv, uint8_t* codes) {
-  uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;
+  uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;  // the fp16 ring's region
   const int gk = a.gk, j = S.Lq_old / gk + gi, p0 = j * gk;
   const int c = threadIdx.x;
+  // the packed segment (head region or page) of the group, and the group's
+  // first token and index in it
+  int t0;
+  uint8_t* seg = a.arena + packed_seg(a.pm, S.head0, a.head_stride, S.seq, h, p0, t0);
+  const int jj = t0 / gk;
 
   // keys: thread c owns channel c of the group's gk tokens
   {
@@ -116,15 +121,15 @@ __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, i
       const double v = half_bits_to_double(token_row(a, S, blk, a.tk, a.K, h, p0 + i)[c]);
       codes[i * kHeadDim + c] = (ok && sv != 0.0) ? (uint8_t)__builtin_rint((v - mn) / sv) : 0;
     }
-    uint16_t* km = reinterpret_cast<uint16_t*>(blk + a.km) + (size_t)j * 2 * kHeadDim;
+    uint16_t* km = reinterpret_cast<uint16_t*>(seg + a.km) + (size_t)jj * 2 * kHeadDim;
     km[c] = sb;
     km[kHeadDim + c] = __builtin_bit_cast(uint16_t, (_Float16)mn);
   }
   __syncthreads();
   if (a.matrix)
-    pack_key_rows_matrix(codes, gk, bk, blk + a.kc + (size_t)p0 * 16 * bk);
+    pack_key_rows_matrix(codes, gk, bk, seg + a.kc + (size_t)t0 * 16 * bk);
   else
-    pack_rows(codes, gk, bk, blk + a.kc + (size_t)p0 * 16 * bk);
+    pack_rows(codes, gk, bk, seg + a.kc + (size_t)t0 * 16 * bk);
   __syncthreads();
 
   // values: one item per (token, value group)
@@ -151,19 +156,19 @@ __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, i
     }
     const uint32_t zb = __builtin_bit_cast(uint16_t, (_Float16)mn);
     if (a.matrix) {
-      uint8_t* vmb = blk + a.vm + (size_t)((p0 + i) / 32) * 128 * ng;
-      const int r = (p0 + i) % 32;
+      uint8_t* vmb = seg + a.vm + (size_t)((t0 + i) / 32) * 128 * ng;
+      const int r = (t0 + i) % 32;
       *reinterpret_cast<uint16_t*>(vmb + value_meta_s(g, r)) = sb;
       *reinterpret_cast<uint16_t*>(vmb + value_meta_z(g, r, ng)) = (uint16_t)zb;
     } else {
-      reinterpret_cast<uint32_t*>(blk + a.vm)[(size_t)(p0 + i) * ng + g] = (uint32_t)sb | (zb << 16);
+      reinterpret_cast<uint32_t*>(seg + a.vm)[(size_t)(t0 + i) * ng + g] = (uint32_t)sb | (zb << 16);
     }
   }
   __syncthreads();
   if (a.matrix)
-    pack_value_blocks_matrix(codes, gk, bv, blk + a.vc + (size_t)p0 * 16 * bv);
+    pack_value_blocks_matrix(codes, gk, bv, seg + a.vc + (size_t)t0 * 16 * bv);
   else
-    pack_rows(codes, gk, bv, blk + a.vc + (size_t)p0 * 16 * bv);
+    pack_rows(codes, gk, bv, seg + a.vc + (size_t)t0 * 16 * bv);
 }
 
 // Copy the new tokens that stay fp16 into the ring of head h.
@@ -195,6 +200,10 @@ __global__ __launch_bounds__(128) void append_kernel(AppendArgs a, int bk, int b
   }
 }
 
+__global__ __launch_bounds__(256) void table_set_kernel(TableSet t) {
+  for (int i = threadIdx.x; i < t.n; i += blockDim.x) t.table[t.idx[i]] = t.val[i];
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = 0u;
@@ -205,6 +214,12 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, size_t n) {
 int launch_append(const AppendArgs& a, int bk, int bv, void* stream) {
   if (a.total_wg <= 0) return 0;
   hipLaunchKernelGGL(append_kernel, dim3(a.total_wg), dim3(128), 0, (hipStream_t)stream, a, bk, bv);
+  return (int)hipGetLastError();
+}
+
+int launch_table_set(const TableSet& t, void* stream) {
+  if (t.n <= 0) return 0;
+  hipLaunchKernelGGL(table_set_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t);
   return (int)hipGetLastError();
 }
 

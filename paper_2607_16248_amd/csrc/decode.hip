@@ -50,13 +50,17 @@ __device__ __forceinline__ uint64_t load_value8(const uint8_t* row, int cc) {
 }
 
 template <int BK, int BV, int GQ>
-__device__ __forceinline__ void packed_group(const DecodeArgs& a, const uint8_t* blk, int j,
+__device__ __forceinline__ void packed_group(const DecodeArgs& a, const DecodeSeq& S, int h, int j,
                                              const float (&qs0)[GQ], const float (&qs1)[GQ],
                                              float* qp, float* p_lds, State<GQ>& st, const int (&lim)[GQ],
                                              int glim, int lane) {
   constexpr int QS = QStride<GQ>::value;
+  // the packed segment (head region or page) holding key group j, and the
+  // group's first token in it
+  int tj;
+  const uint8_t* blk = a.arena + packed_seg(a.pm, S.head0, a.head_stride, S.seq, h, j * a.gk, tj);
   // scales and zeros of the key group: this lane's channels 2*lane, 2*lane+1
-  const uint32_t* km = reinterpret_cast<const uint32_t*>(blk + a.km + (size_t)j * 2 * kHeadDim * 2);
+  const uint32_t* km = reinterpret_cast<const uint32_t*>(blk + a.km + (size_t)(tj / a.gk) * 2 * kHeadDim * 2);
   const uint32_t sw = km[lane], zw = km[kHeadDim / 2 + lane];
   const float s0 = h2f(sw & 0xFFFF), s1 = h2f(sw >> 16), z0 = h2f(zw & 0xFFFF), z1 = h2f(zw >> 16);
   float bias[GQ];
@@ -74,10 +78,11 @@ __device__ __forceinline__ void packed_group(const DecodeArgs& a, const uint8_t*
   const int tq = lane >> 4, cc = lane & 15;
   const int ng = kHeadDim / a.gv, vg = (cc * 8) / a.gv;
   for (int pass = 0; pass < a.gk / 32; ++pass) {
-    const int tbase = j * a.gk + pass * 32;
+    const int tbase = j * a.gk + pass * 32;  // position in the sequence
+    const int tseg = tj + pass * 32;         // position in the packed segment
     // scores: lane pair (2t, 2t+1) splits token t's 128 channels in halves
     uint32_t kw[2 * BK];
-    load_key_half<BK>(blk + a.kc + (size_t)(tbase + tl) * 16 * BK + half * 8 * BK, kw);
+    load_key_half<BK>(blk + a.kc + (size_t)(tseg + tl) * 16 * BK + half * 8 * BK, kw);
     float sig[GQ];
 #pragma unroll
     for (int g = 0; g < GQ; ++g) sig[g] = 0.f;
@@ -106,7 +111,7 @@ __device__ __forceinline__ void packed_group(const DecodeArgs& a, const uint8_t*
     // values: lane (tq, cc) owns channels 8cc..8cc+7 for tokens tq, tq+4, ...
 #pragma unroll 2
     for (int tt = tq; tt < 32; tt += 4) {
-      const int t = tbase + tt;
+      const int t = tseg + tt;
       const uint32_t meta = reinterpret_cast<const uint32_t*>(blk + a.vm)[(size_t)t * ng + vg];
       const float sv = h2f(meta & 0xFFFF), zv = h2f(meta >> 16);
       const uint64_t vb = load_value8<BV>(blk + a.vc + (size_t)t * 16 * BV, cc);
@@ -151,7 +156,7 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
     row_limits<GQ>(a, S, wk.h, wk.rg, lim);
     const int glim = group_limit(a, S, wk.rg);
     for (int j = t0 / a.gk + wv; j < t1 / a.gk; j += kWaves)
-      packed_group<BK, BV, GQ>(a, blk, j, qs0, qs1, qp, pl, st, lim, glim, lane);
+      packed_group<BK, BV, GQ>(a, S, wk.h, j, qs0, qs1, qp, pl, st, lim, glim, lane);
   } else {
     tail_split<GQ>(a, S, wk.h, wk.rg, blk, qs0, qs1, qp, pl, st, lane, wv);
   }

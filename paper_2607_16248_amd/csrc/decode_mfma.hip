@@ -286,8 +286,9 @@ struct MatrixStages {
 };
 
 // CAUSAL: chunk queries (rows see tokens below their own limit); the
-// single-token decode instantiations carry no masking code.
-template <int BK, int BV, int BPG, int GQ, bool CAUSAL>
+// single-token decode instantiations carry no masking code.  PAGED: the
+// packed data live in the pages of a block table (PageMap).
+template <int BK, int BV, int BPG, int GQ, bool CAUSAL, bool PAGED>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MatrixOcc<BK, BV, BPG, GQ>::value))) void
 decode_mfma_kernel(DecodeArgs a) {
   constexpr int NH = MatrixHeads<GQ>::value;  // heads in the score rows
@@ -346,7 +347,24 @@ decode_mfma_kernel(DecodeArgs a) {
   const int col = lane & 15, row = lane >> 4;     // MFMA column, lane row
   const int hc = col >> 2, xc = col & 3, part = col & 1, hs = col / RS;
   const int ng = kHeadDim / a.gv, gsel = xc & (ng - 1);
-  const __amdgpu_buffer_rsrc_t rs = head_rsrc(blk, a.head_stride);
+  // Packed data: the (sequence, head) region, or in a paged cache the pool,
+  // with every block's page found in the block table (a scalar load).
+  constexpr bool paged = PAGED;
+  const __amdgpu_buffer_rsrc_t rs =
+      paged ? head_rsrc(a.arena + a.pm.pool0, a.pm.pool_bytes) : head_rsrc(blk, a.head_stride);
+  const int32_t* ptab = paged ? a.pm.table + (size_t)S.seq * a.pm.max_pages : nullptr;
+  const uint32_t hoff = paged ? (uint32_t)(wk.h * a.pm.page_head_bytes) : 0u;
+  // offset of the segment holding token tok from the resource base, and
+  // tok's position in it
+  auto seg_of = [&](int tok, int& tin) -> uint32_t {
+    if (!paged) {
+      tin = tok;
+      return 0u;
+    }
+    const int pg = tok >> a.pm.page_shift;
+    tin = tok & (a.pm.page_tokens - 1);
+    return (uint32_t)ptab[pg] * (uint32_t)a.pm.page_bytes + hoff;
+  };
   LaneOffsets lo;
   lo.km = 4 * lane;
   lo.kc = col * 16 * BK + row * 4 * BK;
@@ -365,17 +383,23 @@ decode_mfma_kernel(DecodeArgs a) {
   const int vstride = 128 * ng;
   auto load = [&](int i, BlockData<BK, BV>& o) {
     const int j = j0 + kWaves * (i / BPG);
-    const int tok = j * a.gk + (i % BPG) * 32;
-    load_block<BK, BV>(rs, lo, a.km + (uint32_t)j * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
-                       a.vc + (uint32_t)(tok / 32) * 512 * BV, a.vm + (uint32_t)(tok / 32) * vstride, o);
+    int tok;
+    const uint32_t sg = seg_of(j * a.gk + (i % BPG) * 32, tok);
+    const int jg = paged ? tok >> a.pm.gk_shift : j;  // key group within the segment
+    load_block<BK, BV>(rs, lo, sg + a.km + (uint32_t)jg * (2 * kHeadDim * 2), sg + a.kc + (uint32_t)tok * 16 * BK,
+                       sg + a.vc + (uint32_t)(tok / 32) * 512 * BV, sg + a.vm + (uint32_t)(tok / 32) * vstride, o);
   };
   // Key zero-points of the wave's key groups k0 .. k0 + 15 as the A operand
   // of their zero-point terms (row = group; past the last group: the last).
   auto load_z = [&](int k0, h8_t (&zq)[4]) {
-    const uint32_t j = (uint32_t)(j0 + kWaves * min(k0 + col, ngroups - 1));
+    const int j = j0 + kWaves * min(k0 + col, ngroups - 1);
+    int tin;
+    const uint32_t sg = seg_of(j * a.gk, tin);  // per lane in a paged cache
+    const uint32_t jg = paged ? (uint32_t)(tin >> a.pm.gk_shift) : (uint32_t)j;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
-      zq[kb] = __builtin_bit_cast(h8_t, ld128(rs, j * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
+      zq[kb] = __builtin_bit_cast(
+          h8_t, ld128(rs, sg + jg * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
   };
   // the first two blocks and the first zero-points load while the query is prepared
   constexpr int kStages = MatrixStages<BK, BV, BPG, GQ>::value;
@@ -745,14 +769,19 @@ decode_mfma_kernel(DecodeArgs a) {
   write_record<GQ>(a, S, wk.h, wk.rg, wk.sp, red);
 }
 
+template <int BK, int BV, int BPG, int GQ, bool CAUSAL, bool PAGED>
+void launch_k(const DecodeArgs& a, void* stream) {
+  hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG, GQ, CAUSAL, PAGED>), dim3(a.total_wg), dim3(64 * kWaves), 0,
+                     (hipStream_t)stream, a);
+}
+
 template <int BK, int BV, int BPG, int GQ>
 int launch_t(const DecodeArgs& a, void* stream) {
-  if (a.nqry > 1)
-    hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG, GQ, true>), dim3(a.total_wg), dim3(64 * kWaves), 0,
-                       (hipStream_t)stream, a);
-  else
-    hipLaunchKernelGGL((decode_mfma_kernel<BK, BV, BPG, GQ, false>), dim3(a.total_wg), dim3(64 * kWaves), 0,
-                       (hipStream_t)stream, a);
+  const bool causal = a.nqry > 1, paged = a.pm.table != nullptr;
+  if (causal && paged) launch_k<BK, BV, BPG, GQ, true, true>(a, stream);
+  else if (causal) launch_k<BK, BV, BPG, GQ, true, false>(a, stream);
+  else if (paged) launch_k<BK, BV, BPG, GQ, false, true>(a, stream);
+  else launch_k<BK, BV, BPG, GQ, false, false>(a, stream);
   return (int)hipGetLastError();
 }
 

@@ -41,24 +41,26 @@ __device__ __forceinline__ uint32_t value_code_matrix(const uint8_t* block, int 
 __global__ __launch_bounds__(128) void dequant_kernel(DequantArgs a) {
   const int ti = blockIdx.x / a.hkv, h = blockIdx.x % a.hkv;
   const int p = a.tok0 + ti, c = threadIdx.x;
-  const uint8_t* blk = a.base + (uint64_t)h * a.head_stride;
+  const uint8_t* blk = a.arena + a.head0 + (uint64_t)h * a.head_stride;
   float kv, vv;
   if (p < a.Lq) {
-    const uint16_t* km = reinterpret_cast<const uint16_t*>(blk + a.km) + (size_t)(p / a.gk) * 2 * kHeadDim;
-    const uint8_t* krow = blk + a.kc + (size_t)p * 16 * a.bk;
+    int q;  // p's position in its packed segment
+    const uint8_t* seg = a.arena + packed_seg(a.pm, a.head0, a.head_stride, a.seq, h, p, q);
+    const uint16_t* km = reinterpret_cast<const uint16_t*>(seg + a.km) + (size_t)(q / a.gk) * 2 * kHeadDim;
+    const uint8_t* krow = seg + a.kc + (size_t)q * 16 * a.bk;
     const uint32_t kcode = a.matrix ? key_code_matrix(krow, c, a.bk) : code_at(krow, c, a.bk);
     kv = fmaf((float)kcode, h2f(km[c]), h2f(km[kHeadDim + c]));
     const int ng = kHeadDim / a.gv, g = c / a.gv;
     if (a.matrix) {
-      const uint8_t* vblk = blk + a.vc + (size_t)(p / 32) * 512 * a.bv;
-      const uint8_t* vmb = blk + a.vm + (size_t)(p / 32) * 128 * ng;
-      const int r = p % 32;
+      const uint8_t* vblk = seg + a.vc + (size_t)(q / 32) * 512 * a.bv;
+      const uint8_t* vmb = seg + a.vm + (size_t)(q / 32) * 128 * ng;
+      const int r = q % 32;
       const uint32_t vcode = value_code_matrix(vblk, r, c, a.bv);
       vv = fmaf((float)vcode, h2f(*reinterpret_cast<const uint16_t*>(vmb + value_meta_s(g, r))),
                 h2f(*reinterpret_cast<const uint16_t*>(vmb + value_meta_z(g, r, ng))));
     } else {
-      const uint32_t meta = reinterpret_cast<const uint32_t*>(blk + a.vm)[(size_t)p * ng + g];
-      vv = fmaf((float)code_at(blk + a.vc + (size_t)p * 16 * a.bv, c, a.bv), h2f(meta & 0xFFFF), h2f(meta >> 16));
+      const uint32_t meta = reinterpret_cast<const uint32_t*>(seg + a.vm)[(size_t)q * ng + g];
+      vv = fmaf((float)code_at(seg + a.vc + (size_t)q * 16 * a.bv, c, a.bv), h2f(meta & 0xFFFF), h2f(meta >> 16));
     }
   } else {
     const size_t slot = (size_t)(p % a.W) * kHeadDim + c;

@@ -35,6 +35,12 @@ struct kvq_cache {
   std::vector<uint8_t> matrix;  // 1: matrix layout and the matrix-core decode kernel
   std::vector<int> occupancy;    // resident decode workgroups per compute unit, per sequence's kernel
   int32_t split_tokens = 0;
+  // paged layout: block table on the device (pm.table), page lists and the
+  // free pool on the host
+  bool paged = false;
+  kvq::PageMap pm{};
+  std::vector<std::vector<int32_t>> pages;  // per sequence: pool page of each logical page
+  std::vector<int32_t> free_pages;           // taken from the back
 };
 
 namespace {
@@ -102,6 +108,16 @@ kvq_status check_desc(const kvq_cache_desc* d) {
     if (!valid_bits(d->bits_k[i]) || !valid_bits(d->bits_v[i]))
       return fail(KVQ_ERR_ARG, "sequence %d: bits (%d, %d) must each be 1, 2, 4 or 8", i, d->bits_k[i], d->bits_v[i]);
   }
+  const int P = d->page_tokens;
+  if (P < 0 || (P > 0 && (P < d->key_group || P > (1 << 20) || (P & (P - 1)) != 0)))
+    return fail(KVQ_ERR_ARG, "page_tokens %d: must be 0 or a power of two in [key_group = %d, 2^20]", P, d->key_group);
+  if (d->num_pages < 0 || (d->num_pages > 0 && P == 0))
+    return fail(KVQ_ERR_ARG, "num_pages %d: must be >= 0, and 0 unless page_tokens > 0", d->num_pages);
+  if (P > 0) {
+    for (int i = 1; i < d->batch; ++i)
+      if (d->bits_k[i] != d->bits_k[0] || d->bits_v[i] != d->bits_v[0])
+        return fail(KVQ_ERR_UNSUPPORTED, "a paged cache needs one bit width pair for every sequence");
+  }
   return KVQ_OK;
 }
 
@@ -118,6 +134,40 @@ int32_t quantized_len(int64_t L, const kvq_cache_desc& d) {
 HeadLayout layout_of(const kvq_cache_desc* d, int bk, int bv) {
   return kvq::head_layout(bk, bv, packed_capacity(d), d->key_group, d->value_group,
                           (int64_t)d->fp16_window + d->key_group);
+}
+
+// Arena of a paged cache: header | fp16 rings [batch][Hkv] | block table
+// [batch][max_pages] int32 | pool [num_pages][Hkv][page head layout].
+struct PagedArena {
+  HeadLayout page, ring, seq_lay;  // seq_lay: packed offsets of the page, ring offsets and stride
+  uint64_t table_off = 0, pool0 = 0, page_bytes = 0, total = 0;
+  int32_t max_pages = 0, num_pages = 0;
+};
+
+PagedArena paged_arena(const kvq_cache_desc* d) {
+  PagedArena A;
+  const int bk = d->bits_k[0], bv = d->bits_v[0], P = d->page_tokens;
+  const int64_t W = (int64_t)d->fp16_window + d->key_group;
+  A.page = kvq::head_layout(bk, bv, P, d->key_group, d->value_group, 0);
+  A.ring = kvq::head_layout(bk, bv, 0, d->key_group, d->value_group, W);
+  A.seq_lay = A.page;
+  A.seq_lay.tk = A.ring.tk;
+  A.seq_lay.tv = A.ring.tv;
+  A.seq_lay.stride = A.ring.stride;
+  A.max_pages = (int32_t)((packed_capacity(d) + P - 1) / P);
+  A.num_pages = d->num_pages > 0 ? d->num_pages : d->batch * A.max_pages;
+  const uint64_t rings = (uint64_t)d->batch * d->num_kv_heads * A.ring.stride;
+  A.table_off = kvq::align_up(kvq::kHeaderBytes + rings, kvq::kAlign);
+  A.pool0 = kvq::align_up(A.table_off + (uint64_t)d->batch * A.max_pages * 4, kvq::kAlign);
+  A.page_bytes = (uint64_t)d->num_kv_heads * A.page.stride;
+  A.total = A.pool0 + (uint64_t)A.num_pages * A.page_bytes;
+  return A;
+}
+
+int log2_exact(int v) {
+  int s = 0;
+  while ((1 << s) < v) ++s;
+  return s;
 }
 
 // Split length of one launch's sequences (one bit class): the launch fills
@@ -182,6 +232,7 @@ extern "C" {
 
 size_t kvq_cache_bytes(const kvq_cache_desc* d) {
   if (check_desc(d) != KVQ_OK) return 0;
+  if (d->page_tokens > 0) return (size_t)paged_arena(d).total;
   uint64_t total = kvq::kHeaderBytes;
   for (int i = 0; i < d->batch; ++i) total += (uint64_t)d->num_kv_heads * layout_of(d, d->bits_k[i], d->bits_v[i]).stride;
   return (size_t)total;
@@ -208,16 +259,41 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   c->cq = packed_capacity(d);
   c->W = d->fp16_window + d->key_group;
   uint64_t off = kvq::kHeaderBytes;
-  for (int i = 0; i < d->batch; ++i) {
-    c->lay.push_back(layout_of(d, c->bk[i], c->bv[i]));
-    c->head0.push_back(off);
-    off += (uint64_t)d->num_kv_heads * c->lay.back().stride;
+  uint64_t packed_bytes = 0;  // what the matrix kernel's 32-bit offsets must reach
+  if (d->page_tokens > 0) {
+    const PagedArena A = paged_arena(d);
+    c->paged = true;
+    c->pm.table = reinterpret_cast<const int32_t*>(c->arena + A.table_off);
+    c->pm.pool0 = A.pool0;
+    c->pm.page_bytes = A.page_bytes;
+    c->pm.page_head_bytes = A.page.stride;
+    c->pm.pool_bytes = (uint64_t)A.num_pages * A.page_bytes;
+    c->pm.page_tokens = d->page_tokens;
+    c->pm.max_pages = A.max_pages;
+    c->pm.page_shift = log2_exact(d->page_tokens);
+    c->pm.gk_shift = log2_exact(d->key_group);
+    for (int i = 0; i < d->batch; ++i) {
+      c->lay.push_back(A.seq_lay);
+      c->head0.push_back(off);
+      off += (uint64_t)d->num_kv_heads * A.ring.stride;
+    }
+    c->pages.assign(d->batch, {});
+    for (int pg = A.num_pages - 1; pg >= 0; --pg) c->free_pages.push_back(pg);
+    packed_bytes = c->pm.pool_bytes;
+  } else {
+    for (int i = 0; i < d->batch; ++i) {
+      c->lay.push_back(layout_of(d, c->bk[i], c->bv[i]));
+      c->head0.push_back(off);
+      off += (uint64_t)d->num_kv_heads * c->lay.back().stride;
+    }
   }
   c->L.assign(d->batch, 0);
   c->Lq.assign(d->batch, 0);
   for (int i = 0; i < d->batch; ++i)
     c->matrix.push_back(kvq::matrix_decode_supported(c->bk[i], c->bv[i], d->num_q_heads / d->num_kv_heads,
-                                                     d->value_group, c->lay[i].stride) ? 1 : 0);
+                                                     d->value_group, c->paged ? packed_bytes : c->lay[i].stride)
+                            ? 1
+                            : 0);
   // the split plan of a launch fills one round of its kernel's workgroups
   for (int i = 0; i < d->batch; ++i)
     c->occupancy.push_back(c->matrix[i] ? kvq::matrix_decode_occupancy(c->bk[i], c->bv[i], d->key_group,
@@ -235,12 +311,35 @@ kvq_status kvq_cache_reset(kvq_cache* c, void* stream) {
   if (e) return hip_fail(e, "reset");
   std::fill(c->L.begin(), c->L.end(), 0);
   std::fill(c->Lq.begin(), c->Lq.end(), 0);
+  if (c->paged) {
+    for (auto& pl : c->pages) {
+      for (int32_t pg : pl) c->free_pages.push_back(pg);
+      pl.clear();
+    }
+  }
   return ok();
 }
 
 int64_t kvq_seq_len(const kvq_cache* c, int32_t seq) {
   if (!c || seq < 0 || seq >= c->d.batch) return -1;
   return c->L[seq];
+}
+
+kvq_status kvq_seq_release(kvq_cache* c, int32_t seq) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (seq < 0 || seq >= c->d.batch) return fail(KVQ_ERR_ARG, "seq %d out of range", seq);
+  c->L[seq] = 0;
+  c->Lq[seq] = 0;
+  if (c->paged) {
+    for (int32_t pg : c->pages[seq]) c->free_pages.push_back(pg);
+    c->pages[seq].clear();
+  }
+  return ok();
+}
+
+int64_t kvq_free_pages(const kvq_cache* c) {
+  if (!c || !c->paged) return -1;
+  return (int64_t)c->free_pages.size();
 }
 
 kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int32_t n_max, const int32_t* n_new,
@@ -264,11 +363,40 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int32_t n_max,
   std::vector<int> seqs;
   std::vector<int32_t> L_new(d.batch), Lq_new(d.batch);
   bool fused = true;
+  int64_t pages_needed = 0;
   for (int i = 0; i < d.batch; ++i) {
     L_new[i] = c->L[i] + n_new[i];
     Lq_new[i] = quantized_len(L_new[i], d);
     if (n_new[i] > 0) seqs.push_back(i);
     if ((int64_t)L_new[i] - c->Lq[i] > c->W) fused = false;
+    if (c->paged)
+      pages_needed += (Lq_new[i] + d.page_tokens - 1) / d.page_tokens - (int64_t)c->pages[i].size();
+  }
+  if (c->paged && pages_needed > (int64_t)c->free_pages.size())
+    return fail(KVQ_ERR_CAPACITY, "the append needs %lld more pages, the pool has %zu free", (long long)pages_needed,
+                c->free_pages.size());
+  if (c->paged && pages_needed > 0) {
+    // take the pages and write their block-table entries (ordered before the append launch)
+    kvq::TableSet t{};
+    t.table = const_cast<int32_t*>(c->pm.table);
+    for (int i = 0; i < d.batch; ++i) {
+      const int32_t want = (Lq_new[i] + d.page_tokens - 1) / d.page_tokens;
+      while ((int32_t)c->pages[i].size() < want) {
+        const int32_t pg = c->free_pages.back();
+        c->free_pages.pop_back();
+        t.idx[t.n] = i * c->pm.max_pages + (int32_t)c->pages[i].size();
+        t.val[t.n] = pg;
+        ++t.n;
+        c->pages[i].push_back(pg);
+        if (t.n == kvq::kTableSetMax) {
+          const int e = kvq::launch_table_set(t, stream);
+          if (e) return hip_fail(e, "block table launch");
+          t.n = 0;
+        }
+      }
+    }
+    const int e = kvq::launch_table_set(t, stream);
+    if (e) return hip_fail(e, "block table launch");
   }
 
   // fused: one launch packs groups and fills ring slots (no slot is both
@@ -288,6 +416,7 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int32_t n_max,
       a.n_max = n_max; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
       a.quantize = quant ? 1 : 0;
       a.matrix = c->matrix[cls.second[0]];
+      a.pm = c->pm;
       int wg = 0, n = 0;
       for (int i : cls.second) {
         kvq::AppendSeq& s = a.seq[n++];
@@ -421,6 +550,7 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.qscale = qscale;
     const Rows r = rows_for(c, c->matrix[cls.second[0]] != 0, p.nqry);
     a.nqry = r.nqry; a.qpr = r.qpr; a.nrg = r.nrg; a.gqh = d.num_q_heads / d.num_kv_heads;
+    a.pm = c->pm;
     if (app) {
       a.K_new = static_cast<const uint16_t*>(app->K);
       a.V_new = static_cast<const uint16_t*>(app->V);
@@ -577,7 +707,10 @@ kvq_status kvq_dequant(const kvq_cache* c, int32_t seq, int32_t tok0, int32_t nt
   if (!K_out || !V_out) return fail(KVQ_ERR_ARG, "outputs must be device pointers");
   const HeadLayout& lay = c->lay[seq];
   kvq::DequantArgs a{};
-  a.base = c->arena + c->head0[seq];
+  a.arena = c->arena;
+  a.head0 = c->head0[seq];
+  a.seq = seq;
+  a.pm = c->pm;
   a.K_out = K_out; a.V_out = V_out;
   a.head_stride = lay.stride;
   a.kc = (uint32_t)lay.kc; a.km = (uint32_t)lay.km; a.vc = (uint32_t)lay.vc;
@@ -614,7 +747,47 @@ kvq_status kvq_export(const kvq_cache* c, int32_t seq, int32_t h, void* dst, siz
                              {lay.vc, Lq * 16 * c->bv[seq]},
                              {lay.vm, Lq * (D / c->d.value_group) * 4}};
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (c->matrix[seq]) {
+  if (c->paged) {
+    // page by page into the same canonical image: the page's tokens
+    // [t0, t0 + n) of every part, codes and value meta re-ordered by the
+    // export kernel in the matrix layout
+    uint8_t* okc = o;
+    uint8_t* okm = okc + part[0][1];
+    uint8_t* ovc = okm + part[1][1];
+    uint8_t* ovm = ovc + part[2][1];
+    const size_t P = c->d.page_tokens, gk = c->d.key_group, ng = D / c->d.value_group;
+    const int bk = c->bk[seq], bv = c->bv[seq];
+    for (size_t lp = 0; lp * P < Lq; ++lp) {
+      const size_t t0 = lp * P, n = std::min(Lq - t0, P);
+      const uint8_t* seg =
+          c->arena + c->pm.pool0 + (uint64_t)c->pages[seq][lp] * c->pm.page_bytes + (uint64_t)h * c->pm.page_head_bytes;
+      const hipError_t e = hipMemcpyAsync(okm + t0 / gk * 2 * D * 2, seg + lay.km, n / gk * 2 * D * 2,
+                                          hipMemcpyDeviceToDevice, s);
+      if (e != hipSuccess) return hip_fail(e, "export copy");
+      if (c->matrix[seq]) {
+        kvq::ExportArgs x{};
+        x.blk = seg;
+        x.kc_out = okc + t0 * 16 * bk;
+        x.vc_out = ovc + t0 * 16 * bv;
+        x.vm_out = ovm + t0 * ng * 4;
+        x.kc = (uint32_t)lay.kc; x.vc = (uint32_t)lay.vc; x.vm = (uint32_t)lay.vm;
+        x.bk = bk; x.bv = bv; x.gv = c->d.value_group; x.nblocks = (int32_t)(n / 32);
+        const int ek = kvq::launch_export(x, stream);
+        if (ek) return hip_fail(ek, "export launch");
+      } else {
+        const size_t src[3][3] = {{lay.kc, t0 * 16 * bk, n * 16 * bk},
+                                  {lay.vc, t0 * 16 * bv, n * 16 * bv},
+                                  {lay.vm, t0 * ng * 4, n * ng * 4}};
+        uint8_t* dst[3] = {okc, ovc, ovm};
+        for (int k = 0; k < 3; ++k) {
+          const hipError_t e2 = hipMemcpyAsync(dst[k] + src[k][1], seg + src[k][0], src[k][2],
+                                               hipMemcpyDeviceToDevice, s);
+          if (e2 != hipSuccess) return hip_fail(e2, "export copy");
+        }
+      }
+    }
+    o = ovm + part[3][1];
+  } else if (c->matrix[seq]) {
     // key meta is stored canonically; codes and value meta are re-ordered by a kernel
     if (part[1][1]) {
       const hipError_t e = hipMemcpyAsync(o + part[0][1], blk + part[1][0], part[1][1], hipMemcpyDeviceToDevice, s);

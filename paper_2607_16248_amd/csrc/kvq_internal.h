@@ -48,6 +48,53 @@ inline HeadLayout head_layout(int bk, int bv, int64_t cq, int gk, int gv, int64_
   return L;
 }
 
+// ---------------------------------------------------------------- paging
+//
+// Paged caches keep the packed codes and scales of page_tokens consecutive
+// tokens of a sequence (all kv heads) in one page of a shared pool; a block
+// table maps (sequence, logical page) to a pool page.  Within a page, head
+// h's packed data sit at h * page_head_bytes in the head layout of
+// page_tokens tokens.  The fp16 ring of every (sequence, head) stays in a
+// contiguous region of its own.  table == nullptr: contiguous caches.
+struct PageMap {
+  const int32_t* table;      // [batch][max_pages] pool page of each logical page
+  uint64_t pool0;            // arena offset of pool page 0
+  uint64_t page_bytes;       // Hkv * page_head_bytes
+  uint64_t page_head_bytes;
+  uint64_t pool_bytes;       // pages * page_bytes (<= 4 GiB for the matrix kernel)
+  int32_t page_tokens, max_pages;
+  int32_t page_shift, gk_shift;  // log2(page_tokens), log2(key_group)
+};
+
+#ifdef __HIPCC__
+#define KVQ_PAGE_HD __host__ __device__
+#else
+#define KVQ_PAGE_HD
+#endif
+// Arena offset of the packed segment that holds token tok of (sequence seq,
+// kv head h), and tok's position in it.  Contiguous caches: the head's
+// region (head0 + h * head_stride) and tok itself.
+KVQ_PAGE_HD inline uint64_t packed_seg(const PageMap& pm, uint64_t head0, uint64_t head_stride, int seq,
+                                               int h, int tok, int& t_in) {
+  if (pm.table == nullptr) {
+    t_in = tok;
+    return head0 + (uint64_t)h * head_stride;
+  }
+  const int pg = tok >> pm.page_shift;
+  t_in = tok & (pm.page_tokens - 1);
+  return pm.pool0 + (uint64_t)pm.table[(size_t)seq * pm.max_pages + pg] * pm.page_bytes +
+         (uint64_t)h * pm.page_head_bytes;
+}
+
+// Block-table entries written by one launch (graph-safe: no memset/copy node).
+constexpr int kTableSetMax = 240;
+struct TableSet {
+  int32_t* table;
+  int32_t n, pad;
+  int32_t idx[kTableSetMax];
+  int32_t val[kTableSetMax];
+};
+
 // ---------------------------------------------------------------- append
 
 struct AppendSeq {
@@ -68,6 +115,7 @@ struct AppendArgs {
   int32_t n_max, hkv, gk, gv, W, nseq, total_wg;
   int32_t quantize;   // 1: pack groups in this launch
   int32_t matrix;     // 1: matrix layout (kvq_layout.h) for this bit class
+  PageMap pm;
   AppendSeq seq[kMaxSeqPerLaunch];
 };
 
@@ -106,6 +154,7 @@ struct DecodeArgs {
   int32_t hq, hkv, gk, gv, W, split_tokens, nseq, total_wg;
   int32_t nqry, qpr, nrg, gqh;
   float qscale;       // log2(e) / sqrt(d)
+  PageMap pm;
   DecodeSeq seq[kMaxSeqPerLaunch];
 };
 
@@ -148,13 +197,15 @@ struct DgapArgs {
 // ---------------------------------------------------------------- dequant
 
 struct DequantArgs {
-  const uint8_t* base;  // (seq, head 0) block
+  const uint8_t* arena;
+  uint64_t head0;       // (seq, head 0) block (paged: the sequence's ring region)
   float* K_out;
   float* V_out;
   uint64_t head_stride;
   uint32_t kc, km, vc, vm, tk, tv;
   int32_t hkv, gk, gv, W, bk, bv, Lq, tok0, ntok;
-  int32_t matrix;
+  int32_t matrix, seq;
+  PageMap pm;
 };
 
 // ---------------------------------------------------------------- export
@@ -172,6 +223,7 @@ struct ExportArgs {
 
 // Launchers (defined next to their kernels).  Return a hipError_t as int.
 int launch_append(const AppendArgs& a, int bk, int bv, void* stream);
+int launch_table_set(const TableSet& t, void* stream);
 int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
 int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
 // Matrix-core decode (and the matrix layout) for this bit class: 4, 5 or 8

@@ -19,7 +19,8 @@ STATUS_NAMES = ["KVQ_OK", "KVQ_ERR_ARG", "KVQ_ERR_UNSUPPORTED", "KVQ_ERR_CAPACIT
                 "KVQ_ERR_RANGE", "KVQ_ERR_STATE", "KVQ_ERR_HIP"]
 
 EXPORTED = ["kvq_cache_bytes", "kvq_cache_init", "kvq_cache_destroy", "kvq_cache_reset",
-            "kvq_seq_len", "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention", "kvq_append_decode",
+            "kvq_seq_len", "kvq_seq_release", "kvq_free_pages",
+            "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention", "kvq_append_decode",
             "kvq_decode_partials", "kvq_decode_merge", "kvq_chunk_workspace_bytes", "kvq_chunk_attention",
             "kvq_dequant", "kvq_export_bytes", "kvq_export", "kvq_check",
             "kvq_set_split_tokens", "kvq_last_error", "kvq_version",
@@ -38,7 +39,8 @@ class CacheDesc(ctypes.Structure):
                 ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("max_tokens", ctypes.c_int32), ("key_group", ctypes.c_int32),
                 ("value_group", ctypes.c_int32), ("fp16_window", ctypes.c_int32),
-                ("bits_k", ctypes.POINTER(ctypes.c_uint8)), ("bits_v", ctypes.POINTER(ctypes.c_uint8))]
+                ("bits_k", ctypes.POINTER(ctypes.c_uint8)), ("bits_v", ctypes.POINTER(ctypes.c_uint8)),
+                ("page_tokens", ctypes.c_int32), ("num_pages", ctypes.c_int32)]
 
 
 class DgapParams(ctypes.Structure):
@@ -70,6 +72,8 @@ def lib():
         "kvq_cache_destroy": ([P], None),
         "kvq_cache_reset": ([P, P], ctypes.c_int),
         "kvq_seq_len": ([P, I32], I64),
+        "kvq_seq_release": ([P, I32], ctypes.c_int),
+        "kvq_free_pages": ([P], I64),
         "kvq_append": ([P, P, P, I32, ctypes.POINTER(I32), P], ctypes.c_int),
         "kvq_workspace_bytes": ([P], S),
         "kvq_decode_attention": ([P, P, P, P, S, P], ctypes.c_int),
@@ -124,13 +128,13 @@ def _stream(stream) -> Optional[int]:
 
 def make_desc(batch: int, num_q_heads: int, num_kv_heads: int, head_dim: int, max_tokens: int,
               key_group: int, value_group: int, fp16_window: int, bits_k: Sequence[int],
-              bits_v: Sequence[int]):
+              bits_v: Sequence[int], page_tokens: int = 0, num_pages: int = 0):
     """A descriptor plus the host arrays it points to (keep both alive)."""
     bk = (ctypes.c_uint8 * max(1, len(bits_k)))(*bits_k)
     bv = (ctypes.c_uint8 * max(1, len(bits_v)))(*bits_v)
     d = CacheDesc(batch, num_q_heads, num_kv_heads, head_dim, max_tokens, key_group, value_group,
                   fp16_window, ctypes.cast(bk, ctypes.POINTER(ctypes.c_uint8)),
-                  ctypes.cast(bv, ctypes.POINTER(ctypes.c_uint8)))
+                  ctypes.cast(bv, ctypes.POINTER(ctypes.c_uint8)), page_tokens, num_pages)
     d._keep = (bk, bv)
     return d
 
@@ -158,6 +162,14 @@ def kvq_cache_reset(cache: int, stream=None) -> None:
 
 def kvq_seq_len(cache: int, seq: int) -> int:
     return int(lib().kvq_seq_len(cache, seq))
+
+
+def kvq_seq_release(cache: int, seq: int) -> None:
+    _check(lib().kvq_seq_release(cache, seq))
+
+
+def kvq_free_pages(cache: int) -> int:
+    return int(lib().kvq_free_pages(cache))
 
 
 def kvq_append(cache: int, K, V, n_new: Sequence[int], n_max: Optional[int] = None, stream=None) -> None:
@@ -250,12 +262,14 @@ class KVCache:
     """A cache over a torch-allocated, zero-filled device arena."""
 
     def __init__(self, batch, num_q_heads, num_kv_heads, max_tokens, bits_k, bits_v,
-                 key_group=32, value_group=32, fp16_window=0, head_dim=128, device="cuda"):
+                 key_group=32, value_group=32, fp16_window=0, head_dim=128, device="cuda",
+                 page_tokens=0, num_pages=0):
         import torch
         bits_k = list(bits_k) if hasattr(bits_k, "__len__") else [bits_k] * batch
         bits_v = list(bits_v) if hasattr(bits_v, "__len__") else [bits_v] * batch
         self.desc = make_desc(batch, num_q_heads, num_kv_heads, head_dim, max_tokens, key_group,
-                              value_group, fp16_window, bits_k, bits_v)
+                              value_group, fp16_window, bits_k, bits_v, page_tokens, num_pages)
+        self.page_tokens, self.num_pages = page_tokens, num_pages
         self.batch, self.num_q_heads, self.num_kv_heads = batch, num_q_heads, num_kv_heads
         self.head_dim, self.key_group, self.value_group = head_dim, key_group, value_group
         self.fp16_window, self.bits_k, self.bits_v, self.max_tokens = fp16_window, bits_k, bits_v, max_tokens
@@ -320,6 +334,12 @@ class KVCache:
 
     def seq_len(self, seq):
         return kvq_seq_len(self.handle, seq)
+
+    def release(self, seq):
+        kvq_seq_release(self.handle, seq)
+
+    def free_pages(self):
+        return kvq_free_pages(self.handle)
 
     def export(self, seq, kv_head):
         import torch

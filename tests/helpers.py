@@ -32,7 +32,7 @@ class Case:
     """Seeded inputs for a batch plus a cache holding them."""
 
     def __init__(self, w: Workload, layer: int = 0, heads: Optional[List[int]] = None,
-                 device: str = "cuda", max_tokens: Optional[int] = None):
+                 device: str = "cuda", max_tokens: Optional[int] = None, **cache_kw):
         import torch
         self.w = w
         self.heads = heads
@@ -45,7 +45,7 @@ class Case:
         self.cache = kvq.KVCache(w.batch, w.num_q_heads, w.num_kv_heads,
                                  max_tokens or max(max(w.lens), 1), list(w.bits_k), list(w.bits_v),
                                  key_group=w.key_group, value_group=w.value_group,
-                                 fp16_window=w.window, device=device)
+                                 fp16_window=w.window, device=device, **cache_kw)
         self.qd = torch.from_numpy(np.stack(self.q)).to(device)
 
     def append_all(self, chunks: Optional[Sequence[int]] = None):

@@ -190,6 +190,49 @@ def test_split_setting_and_workspace_bound():
         kvq.kvq_cache_destroy(h)
 
 
+@pytest.mark.parametrize("kw,status", [
+    (dict(page_tokens=48), "ARG"),                         # not a power of two
+    (dict(page_tokens=16), "ARG"),                         # below key_group
+    (dict(page_tokens=-64), "ARG"),
+    (dict(num_pages=4), "ARG"),                            # a pool without pages
+    (dict(page_tokens=64, num_pages=-1), "ARG"),
+    (dict(page_tokens=64, batch=2, bits_k=[1, 2], bits_v=[1, 2]), "UNSUPPORTED"),
+])
+def test_paged_descriptor_errors(kw, status):
+    d = desc(**kw)
+    assert kvq.kvq_cache_bytes(d) == 0
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.kvq_cache_init(d, FAKE_ARENA, 1 << 30)
+    assert e.value.status == getattr(kvq, "ERR_" + status)
+
+
+def test_paged_pool_size_and_capacity_errors():
+    # K1V1, 8 kv heads, pages of 256 tokens: 4 KiB of codes, 4 KiB of key
+    # scales, 4 KiB of value codes and 4 KiB of value scales per head
+    base = desc(max_tokens=4096, bits_k=[1], bits_v=[1], page_tokens=256, num_pages=3)
+    more = desc(max_tokens=4096, bits_k=[1], bits_v=[1], page_tokens=256, num_pages=4)
+    assert kvq.kvq_cache_bytes(more) - kvq.kvq_cache_bytes(base) == 8 * 4 * 4096
+    full = desc(max_tokens=4096, bits_k=[1], bits_v=[1], page_tokens=256)
+    assert kvq.kvq_cache_bytes(full) - kvq.kvq_cache_bytes(base) == 13 * 8 * 4 * 4096   # 16 pages by default
+    h = kvq.kvq_cache_init(base, FAKE_ARENA, kvq.kvq_cache_bytes(base))
+    try:
+        assert kvq.kvq_free_pages(h) == 3
+        # 1000 tokens pack 992 (31 key groups): 4 pages, one more than the pool
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.kvq_append(h, FAKE_ARENA, FAKE_ARENA, [1000], n_max=1000)
+        assert e.value.status == kvq.ERR_CAPACITY and "pages" in kvq.kvq_last_error()
+        assert kvq.kvq_seq_len(h, 0) == 0 and kvq.kvq_free_pages(h) == 3
+        kvq.kvq_seq_release(h, 0)
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.kvq_seq_release(h, 1)
+        assert e.value.status == kvq.ERR_ARG
+    finally:
+        kvq.kvq_cache_destroy(h)
+    c = kvq.kvq_cache_init(desc(), FAKE_ARENA, kvq.kvq_cache_bytes(desc()))
+    assert kvq.kvq_free_pages(c) == -1
+    kvq.kvq_cache_destroy(c)
+
+
 def test_chunk_attention_sizes_and_argument_errors():
     """Every check of kvq_chunk_attention precedes any launch."""
     d = desc(max_tokens=4096, bits_k=[1], bits_v=[1])
