@@ -14,7 +14,9 @@ The line also carries "dgap": DGAP's logit-side step (features, detector,
 top-K window, corrector, merge) on one logit row of the workload's model
 vocabulary, timed on its own (--no-dgap skips it), and "chunk": the last
 4 / 16 / 64 tokens attending causally over the same caches
-(kvq_chunk_attention; --no-chunk skips it).
+(kvq_chunk_attention; --no-chunk skips it), and "paged": the split kernel
+over 8 layers held in 256-token pages against the same layers held
+contiguously (--no-paged skips it).
 """
 from __future__ import annotations
 
@@ -210,6 +212,61 @@ def chunk_leg(handles, w, launch_bytes: int, stream, iters: int):
     return out
 
 
+PAGE_TOKENS = 256
+
+
+def paged_leg(w, qs, dev, stream, iters: int, nlayers: int = 8):
+    """The split kernel over paged caches (pages of PAGE_TOKENS tokens from a
+    shared pool, block table per sequence) against contiguous caches holding
+    the same seeded tokens: nlayers of each, rotating, HIP events on the
+    launch stream; and the decode outputs of the two compared bit for bit."""
+    import torch
+
+    from paper_2607_16248_amd import kvq
+    from workloads import gen_kv_device
+
+    sets = {}
+    for name, P in (("contiguous", 0), ("paged", PAGE_TOKENS)):
+        cs = []
+        for l in range(nlayers):
+            c = kvq.KVCache(w.batch, w.num_q_heads, w.num_kv_heads, max(w.lens), list(w.bits_k), list(w.bits_v),
+                            key_group=w.key_group, value_group=w.value_group, fp16_window=w.window, device=dev,
+                            page_tokens=P)
+            Kb = torch.zeros((w.batch, max(w.lens), w.num_kv_heads, w.head_dim), dtype=torch.float16, device=dev)
+            Vb = torch.zeros_like(Kb)
+            for s in range(w.batch):
+                K, V = gen_kv_device(w, l, s, w.lens[s], dev, torch)
+                Kb[s, :w.lens[s]] = K
+                Vb[s, :w.lens[s]] = V
+                del K, V
+            c.append(Kb, Vb, list(w.lens))
+            del Kb, Vb
+            cs.append(c)
+        sets[name] = cs
+    torch.cuda.synchronize()
+    out = {"page_tokens": PAGE_TOKENS, "layers": nlayers}
+    outs = {}
+    for name, cs in sets.items():
+        ws_bytes = max(kvq.kvq_workspace_bytes(c.handle) for c in cs)
+        ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+        for i in range(8):
+            kvq.kvq_decode_partials(cs[i % nlayers].handle, qs[i % nlayers], ws, ws_bytes, stream=stream)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for i in range(iters):
+            kvq.kvq_decode_partials(cs[i % nlayers].handle, qs[i % nlayers], ws, ws_bytes, stream=stream)
+        b.record()
+        torch.cuda.synchronize()
+        out[f"split_us_{name}"] = round(a.elapsed_time(b) * 1e3 / iters, 3)
+        o = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+        cs[0].decode(qs[0], o)
+        torch.cuda.synchronize()
+        outs[name] = o
+    out["outputs_bit_identical"] = bool(torch.equal(outs["contiguous"], outs["paged"]))
+    return out
+
+
 def dgap_cpu_baseline(workload_idx: int, bits: int) -> float:
     """Part of the CPU-baseline leg: the DGAP oracle (fp64, one thread) on the
     same row, microseconds per corrected step."""
@@ -238,6 +295,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dgap", action="store_true", help="skip the DGAP logit-side leg")
     ap.add_argument("--no-chunk", action="store_true", help="skip the chunk-query leg")
+    ap.add_argument("--no-paged", action="store_true", help="skip the paged-cache leg")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="end with 4 plain device copies of 256 MiB (counter calibration)")
     args = ap.parse_args()
@@ -491,6 +549,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if not args.no_paged:
+        log("[bench] paged caches")
+        result["paged"] = paged_leg(w, qs, dev, stream, 64)
     if not args.no_chunk:
         log("[bench] chunk queries")
         result["chunk"] = chunk_leg(handles, w, launch_bytes, stream, max(2 * layers, 32))

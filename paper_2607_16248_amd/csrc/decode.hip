@@ -105,7 +105,7 @@ __device__ __forceinline__ void packed_group(const DecodeArgs& a, const DecodeSe
       for (int g = 0; g < GQ; ++g)
         if (tbase + tl >= lim[g]) sig[g] = -__builtin_inff();
     }
-    softmax_pass<GQ>(st, sig, half, tl, p_lds);
+    softmax_pass<GQ, true>(st, sig, half, tl, p_lds);
     wave_lds_sync();
 
     // values: lane (tq, cc) owns channels 8cc..8cc+7 for tokens tq, tq+4, ...
@@ -137,13 +137,13 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
   __shared__ float p_lds[kWaves][32 * GQ];
   __shared__ Reduce<GQ> red;
 
-  const Work wk = find_work(a);
+  const Work wk = find_work<true>(a);
   const DecodeSeq& S = a.seq[wk.si];
   const uint8_t* blk = a.arena + S.head0 + (uint64_t)wk.h * a.head_stride;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
 
   float qs0[GQ], qs1[GQ];
-  load_q_scaled<GQ>(a, S, wk.h, wk.rg, lane, qs0, qs1);
+  load_q_scaled<GQ, true>(a, S, wk.h, wk.rg, lane, qs0, qs1);
   State<GQ> st;
   init_state<GQ>(st);
 
@@ -158,11 +158,11 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
     for (int j = t0 / a.gk + wv; j < t1 / a.gk; j += kWaves)
       packed_group<BK, BV, GQ>(a, S, wk.h, j, qs0, qs1, qp, pl, st, lim, glim, lane);
   } else {
-    tail_split<GQ>(a, S, wk.h, wk.rg, blk, qs0, qs1, qp, pl, st, lane, wv);
+    tail_split<GQ, true>(a, S, wk.h, wk.rg, blk, qs0, qs1, qp, pl, st, lane, wv);
   }
   stage_state<GQ>(st, red, lane, wv);
   __syncthreads();
-  write_record<GQ>(a, S, wk.h, wk.rg, wk.sp, red);
+  write_record<GQ, true>(a, S, wk.h, wk.rg, wk.sp, red);
 }
 
 // One workgroup per (sequence, query head, 32-channel slice): thread

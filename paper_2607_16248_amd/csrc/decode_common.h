@@ -74,15 +74,16 @@ struct State {
 
 // Online-softmax update for one pass of 32 tokens held as sig (QK layout:
 // lanes 2t, 2t+1 hold token t).  Writes p to LDS, rescales the state.
-template <int GQ>
+template <int GQ, bool CHUNK>
 __device__ __forceinline__ void softmax_pass(State<GQ>& st, float (&sig)[GQ], int half, int tl,
                                              float* p_lds) {
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
     const float mx = wave_max(sig[g]);
     const float mnew = fmaxf(st.m[g], mx);
-    // a row with no visible token yet keeps m = -inf: factor 1, weights 0
-    const bool none = mnew == -__builtin_inff();
+    // a chunk row with no visible token yet keeps m = -inf: factor 1,
+    // weights 0 (single-token decode sees a token in every pass)
+    const bool none = CHUNK && mnew == -__builtin_inff();
     const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(st.m[g] - mnew);
     const float p = none ? 0.f : __builtin_amdgcn_exp2f(sig[g] - mnew);
     st.l[g] = st.l[g] * alpha + (half ? 0.f : p);
@@ -94,7 +95,7 @@ __device__ __forceinline__ void softmax_pass(State<GQ>& st, float (&sig)[GQ], in
 }
 
 // fp16 tail tokens [Lq, L), read from the ring; pass `pass` covers 32 tokens.
-template <int GQ>
+template <int GQ, bool CHUNK>
 __device__ __forceinline__ void tail_pass(const DecodeArgs& a, const DecodeSeq& S, const uint8_t* blk,
                                           int pass, const float* qp, float* p_lds, State<GQ>& st,
                                           const int (&lim)[GQ], int lane) {
@@ -124,9 +125,9 @@ __device__ __forceinline__ void tail_pass(const DecodeArgs& a, const DecodeSeq& 
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
     sig[g] += dpp_mov<kQuadXor1>(0.f, sig[g]);
-    if (idx >= ntail || S.Lq + idx >= lim[g]) sig[g] = -__builtin_inff();
+    if (idx >= ntail || (CHUNK && S.Lq + idx >= lim[g])) sig[g] = -__builtin_inff();
   }
-  softmax_pass<GQ>(st, sig, half, tl, p_lds);
+  softmax_pass<GQ, CHUNK>(st, sig, half, tl, p_lds);
   wave_lds_sync();
   const int tq = lane >> 4, cc = lane & 15;
   for (int tt = tq; tt < 32; tt += 4) {
@@ -151,34 +152,40 @@ struct Work {
   int si, h, rg, sp;
 };
 
+// CHUNK = false: single-token decode (one query, one row group of the kv
+// head's GQ query heads), where the row arithmetic reduces to h * GQ + g.
+template <bool CHUNK>
 __device__ __forceinline__ Work find_work(const DecodeArgs& a) {
   const int wg = blockIdx.x;
   int si = 0;
   for (int i = 1; i < a.nseq; ++i) si = (a.seq[i].wg_begin <= wg) ? i : si;
   const int local = wg - a.seq[si].wg_begin;
   const int hv = local / a.seq[si].nsplit;
-  return {si, hv / a.nrg, hv % a.nrg, local % a.seq[si].nsplit};
+  Work w{si, hv, 0, local % a.seq[si].nsplit};
+  if (CHUNK && a.nrg > 1) {  // chunk queries: kv head and row group
+    w.h = hv / a.nrg;
+    w.rg = hv - w.h * a.nrg;
+  }
+  return w;
 }
 
-// Row g of the workgroup's row group: chunk query j, query head hd.
-struct QueryRow {
-  int j, hd;
-};
-
-__device__ __forceinline__ QueryRow query_row(const DecodeArgs& a, int h, int rg, int g) {
-  const int x = g / a.gqh;
-  return {rg * a.qpr + x, h * a.gqh + (g - x * a.gqh)};
-}
-
-// Query row g in q / out ([batch][nqry][Hq]).
+// Row g of the workgroup's row group: its index in q / out
+// ([batch][nqry][Hq]), its record row within a split (query * Hq + head),
+// and the end of the tokens it sees.
+template <int GQ, bool CHUNK>
 __device__ __forceinline__ size_t q_index(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int g) {
-  const QueryRow r = query_row(a, h, rg, g);
-  return ((size_t)S.seq * a.nqry + r.j) * a.hq + r.hd;
+  if constexpr (!CHUNK) return (size_t)S.seq * a.hq + (size_t)h * GQ + g;
+  return ((size_t)S.seq * a.nqry + rg * a.qpr) * a.hq + h * a.gqh + a.row_off[g];
 }
 
-// Tokens [0, limit) are visible to row g.
-__device__ __forceinline__ int row_limit(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int g) {
-  return S.L - a.nqry + 1 + query_row(a, h, rg, g).j;
+template <int GQ, bool CHUNK>
+__device__ __forceinline__ int rec_row(const DecodeArgs& a, int h, int rg, int g) {
+  if constexpr (!CHUNK) return h * GQ + g;
+  return rg * a.qpr * a.hq + h * a.gqh + a.row_off[g];
+}
+
+__device__ __forceinline__ int row_limit(const DecodeArgs& a, const DecodeSeq& S, int rg, int g) {
+  return S.L - a.nqry + 1 + rg * a.qpr + a.row_x[g];
 }
 
 // The smallest limit of the row group: every token below it is visible to
@@ -190,7 +197,7 @@ __device__ __forceinline__ int group_limit(const DecodeArgs& a, const DecodeSeq&
 template <int GQ>
 __device__ __forceinline__ void row_limits(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int (&lim)[GQ]) {
 #pragma unroll
-  for (int g = 0; g < GQ; ++g) lim[g] = row_limit(a, S, h, rg, g);
+  for (int g = 0; g < GQ; ++g) lim[g] = row_limit(a, S, rg, g);
 }
 
 // Per-wave partial results of GQ query heads, staged for the combine.
@@ -227,7 +234,7 @@ __device__ __forceinline__ void stage_state(State<GQ>& st, Reduce<GQ>& r, int la
 
 // After a barrier: merge the waves' partial results and write the record of
 // split sp for the GQ query heads of kv head h.
-template <int GQ>
+template <int GQ, bool CHUNK>
 __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int sp,
                                              const Reduce<GQ>& r) {
   for (int idx = threadIdx.x; idx < GQ * kHeadDim; idx += blockDim.x) {
@@ -238,20 +245,22 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSe
     float val = 0.f, lsum = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
-      // a wave that saw no visible token of the row has m = -inf, l = 0
-      const float f = r.m[w][g] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(r.m[w][g] - M);
+      // a wave that saw no visible token of a chunk row has m = -inf, l = 0
+      // (in single-token decode some wave of every split has a block, so M
+      // is finite and exp2(-inf - M) = 0 already)
+      const float f = CHUNK && r.m[w][g] == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(r.m[w][g] - M);
       val = fmaf(f, r.acc[w][idx], val);
       lsum = fmaf(f, r.l[w][g], lsum);
     }
-    const QueryRow qr = query_row(a, h, rg, g);
-    float* rec = a.ws + ((size_t)(S.ws_base + sp) * a.hq * a.nqry + (size_t)qr.j * a.hq + qr.hd) * kRecFloats;
+    const size_t rows = CHUNK ? (size_t)a.hq * a.nqry : (size_t)a.hq;
+    float* rec = a.ws + ((size_t)(S.ws_base + sp) * rows + rec_row<GQ, CHUNK>(a, h, rg, g)) * kRecFloats;
     rec[4 + c] = val;
     if (c == 0) { rec[0] = M; rec[1] = lsum; }
   }
 }
 
 // The fp16 tail split: every wave takes passes of 32 tokens.
-template <int GQ>
+template <int GQ, bool CHUNK>
 __device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq& S, int h, int rg,
                                            const uint8_t* blk, const float (&qs0)[GQ], const float (&qs1)[GQ],
                                            float* qp, float* pl, State<GQ>& st, int lane, int wv) {
@@ -282,7 +291,8 @@ __device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq&
   wave_lds_sync();
   int lim[GQ];
   row_limits<GQ>(a, S, h, rg, lim);
-  for (int pass = wv; pass * 32 < S.L - S.Lq; pass += kWaves) tail_pass<GQ>(a, S, blk, pass, qp, pl, st, lim, lane);
+  for (int pass = wv; pass * 32 < S.L - S.Lq; pass += kWaves)
+    tail_pass<GQ, CHUNK>(a, S, blk, pass, qp, pl, st, lim, lane);
 }
 
 template <int GQ>
@@ -298,12 +308,12 @@ __device__ __forceinline__ void init_state(State<GQ>& st) {
 
 // This lane's two channels (2*lane, 2*lane+1) of the GQ query heads,
 // pre-scaled to base 2.
-template <int GQ>
+template <int GQ, bool CHUNK>
 __device__ __forceinline__ void load_q_scaled(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int lane,
                                               float (&qs0)[GQ], float (&qs1)[GQ]) {
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + q_index(a, S, h, rg, g) * kHeadDim)[lane];
+    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + q_index<GQ, CHUNK>(a, S, h, rg, g) * kHeadDim)[lane];
     qs0[g] = h2f(w & 0xFFFF) * a.qscale;
     qs1[g] = h2f(w >> 16) * a.qscale;
   }

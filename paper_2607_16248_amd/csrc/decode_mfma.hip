@@ -307,7 +307,7 @@ decode_mfma_kernel(DecodeArgs a) {
   constexpr int kTabWords = BV == 1 ? 256 * 4 : BV == 2 ? 256 * 2 : 4;
   __shared__ __attribute__((aligned(16))) uint32_t vtab[kTabWords];
 
-  const Work wk = find_work(a);
+  const Work wk = find_work<CAUSAL>(a);
   const DecodeSeq& S = a.seq[wk.si];
   const uint8_t* blk = a.arena + S.head0 + (uint64_t)wk.h * a.head_stride;
   // wave index as a scalar so that per-wave loop bounds stay in SGPRs
@@ -330,15 +330,16 @@ decode_mfma_kernel(DecodeArgs a) {
 
   if (wk.sp >= S.nq) {  // fp16 tail tokens: vector path
     float qs0[GQ], qs1[GQ];
-    load_q_scaled<GQ>(a, S, wk.h, wk.rg, lane, qs0, qs1);
+    load_q_scaled<GQ, CAUSAL>(a, S, wk.h, wk.rg, lane, qs0, qs1);
     State<GQ> st;
     init_state<GQ>(st);
     static_assert(kHeadDim * QStride<GQ>::value <= (3 * NH + kDzRows) * kQRow, "tail query fits the Q' area");
     static_assert(32 * GQ <= kPRow * NH, "tail weights fit the weight area");
-    tail_split<GQ>(a, S, wk.h, wk.rg, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st, lane, wv);
+    tail_split<GQ, CAUSAL>(a, S, wk.h, wk.rg, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st,
+                           lane, wv);
     stage_state<GQ>(st, red, lane, wv);
     __syncthreads();
-    write_record<GQ>(a, S, wk.h, wk.rg, wk.sp, red);
+    write_record<GQ, CAUSAL>(a, S, wk.h, wk.rg, wk.sp, red);
     return;
   }
 
@@ -347,6 +348,9 @@ decode_mfma_kernel(DecodeArgs a) {
   const int col = lane & 15, row = lane >> 4;     // MFMA column, lane row
   const int hc = col >> 2, xc = col & 3, part = col & 1, hs = col / RS;
   const int ng = kHeadDim / a.gv, gsel = xc & (ng - 1);
+  // row g of the row group reads q row qbase + row_off[g] (row_off[0] = 0)
+  const uint16_t* qbase = CAUSAL ? a.q + q_index<GQ, CAUSAL>(a, S, wk.h, wk.rg, 0) * kHeadDim
+                                 : a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * GQ) * kHeadDim;
   // Packed data: the (sequence, head) region, or in a paged cache the pool,
   // with every block's page found in the block table (a scalar load).
   constexpr bool paged = PAGED;
@@ -431,7 +435,7 @@ decode_mfma_kernel(DecodeArgs a) {
   }
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + q_index(a, S, wk.h, wk.rg, g) * kHeadDim)[lane];
+    const uint32_t w = reinterpret_cast<const uint32_t*>(qbase + (size_t)(CAUSAL ? a.row_off[g] : g) * kHeadDim)[lane];
     const float q0 = h2f(w & 0xFFFF), q1 = h2f(w >> 16);
     const float mx = wave_max(fmaxf(fabsf(q0), fabsf(q1)));
     int e = 0;
@@ -456,7 +460,7 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
   for (int hh = 0; hh < HPL; ++hh) {
     const int g = HPL * row + hh;
-    lim[hh] = g < GQ ? row_limit(a, S, wk.h, wk.rg, g) : S.L;
+    lim[hh] = g < GQ ? row_limit(a, S, wk.rg, g) : S.L;
   }
 
   // Zero-point terms sum_c z[c] q~[c] of 16 key groups and the NH heads, in
@@ -595,8 +599,9 @@ decode_mfma_kernel(DecodeArgs a) {
         b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
         b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
         const float mnew = b > m[hh] ? b + kLazyMargin : m[hh];
-        // 1 where the reference stays (also a row with no visible token yet)
-        alpha[hh] = mnew == m[hh] ? 1.f : __builtin_amdgcn_exp2f(m[hh] - mnew);
+        // 1 where the reference stays; a chunk row with no visible token yet
+        // keeps m = -inf (single-token rows all move at the first block)
+        alpha[hh] = CAUSAL && mnew == m[hh] ? 1.f : __builtin_amdgcn_exp2f(m[hh] - mnew);
         l[hh] *= alpha[hh];
         m[hh] = mnew;
       }
@@ -766,7 +771,7 @@ decode_mfma_kernel(DecodeArgs a) {
     }
   }
   __syncthreads();
-  write_record<GQ>(a, S, wk.h, wk.rg, wk.sp, red);
+  write_record<GQ, CAUSAL>(a, S, wk.h, wk.rg, wk.sp, red);
 }
 
 template <int BK, int BV, int BPG, int GQ, bool CAUSAL, bool PAGED>

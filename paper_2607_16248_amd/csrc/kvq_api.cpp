@@ -550,6 +550,10 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.qscale = qscale;
     const Rows r = rows_for(c, c->matrix[cls.second[0]] != 0, p.nqry);
     a.nqry = r.nqry; a.qpr = r.qpr; a.nrg = r.nrg; a.gqh = d.num_q_heads / d.num_kv_heads;
+    for (int g = 0; g < 8; ++g) {
+      a.row_x[g] = g / a.gqh;
+      a.row_off[g] = a.row_x[g] * d.num_q_heads + g % a.gqh;
+    }
     a.pm = c->pm;
     if (app) {
       a.K_new = static_cast<const uint16_t*>(app->K);

@@ -152,10 +152,16 @@ struct DecodeArgs {
   uint64_t head_stride;
   uint32_t kc, km, vc, vm, tk, tv;
   int32_t hq, hkv, gk, gv, W, split_tokens, nseq, total_wg;
-  int32_t nqry, qpr, nrg, gqh;
   float qscale;       // log2(e) / sqrt(d)
-  PageMap pm;
   DecodeSeq seq[kMaxSeqPerLaunch];
+  // (read by chunk and paged launches only; after the per-sequence entries
+  // so that single-token decode reads the same argument lines as before)
+  int32_t nqry, qpr, nrg, gqh;
+  // row g of a row group is chunk query rg*qpr + row_x[g] and head
+  // h*gqh + (row_off[g] - row_x[g]*Hq): row_off[g] = row_x[g]*Hq + g % gqh
+  // (host-computed, so the kernels divide nothing)
+  int32_t row_off[8], row_x[8];
+  PageMap pm;
 };
 
 struct MergeSeq {
