@@ -536,7 +536,7 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
-            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.key_group // 32},{w.group_q},false>" if matrix_path(w) else
+            "kernel": (f"decode_mfma_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.key_group // 32},{w.group_q},false,false>" if matrix_path(w) else
                        f"decode_split_kernel<{w.bits_k[0]},{w.bits_v[0]},{w.group_q}>"),
             "bytes_per_launch": launch_bytes,
             "kernel_source_sha256_16": source_digest(),
