@@ -352,15 +352,34 @@ decode_mfma_kernel(DecodeArgs a) {
   const uint16_t* qbase = CAUSAL ? a.q + q_index<GQ, CAUSAL>(a, S, wk.h, wk.rg, 0) * kHeadDim
                                  : a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * GQ) * kHeadDim;
   // Packed data: the (sequence, head) region, or in a paged cache the pool,
-  // with every block's page found in the block table (a scalar load).
+  // with every block's page taken from the block table.  The split's first
+  // 64 pages are loaded once, one per lane; a block reads its page's offset
+  // from that lane (pages further on, in splits of more than 64 pages, come
+  // from the table directly).
   constexpr bool paged = PAGED;
   const __amdgpu_buffer_rsrc_t rs =
       paged ? head_rsrc(a.arena + a.pm.pool0, a.pm.pool_bytes) : head_rsrc(blk, a.head_stride);
   const int32_t* ptab = paged ? a.pm.table + (size_t)S.seq * a.pm.max_pages : nullptr;
   const uint32_t hoff = paged ? (uint32_t)(wk.h * a.pm.page_head_bytes) : 0u;
+  const int pg0 = paged ? (wk.sp * a.split_tokens) >> a.pm.page_shift : 0;
+  uint32_t lane_pg = 0u;
+  if constexpr (PAGED) {
+    if (pg0 + lane < a.pm.max_pages) lane_pg = (uint32_t)ptab[pg0 + lane] * (uint32_t)a.pm.page_bytes + hoff;
+  }
   // offset of the segment holding token tok from the resource base, and
-  // tok's position in it
+  // tok's position in it; seg_of takes a wave-uniform token
   auto seg_of = [&](int tok, int& tin) -> uint32_t {
+    if (!paged) {
+      tin = tok;
+      return 0u;
+    }
+    const int pg = tok >> a.pm.page_shift;
+    tin = tok & (a.pm.page_tokens - 1);
+    const int k = pg - pg0;
+    return k < 64 ? (uint32_t)__builtin_amdgcn_readlane((int)lane_pg, k)
+                  : (uint32_t)ptab[pg] * (uint32_t)a.pm.page_bytes + hoff;
+  };
+  auto seg_of_lane = [&](int tok, int& tin) -> uint32_t {  // per-lane token
     if (!paged) {
       tin = tok;
       return 0u;
@@ -398,7 +417,7 @@ decode_mfma_kernel(DecodeArgs a) {
   auto load_z = [&](int k0, h8_t (&zq)[4]) {
     const int j = j0 + kWaves * min(k0 + col, ngroups - 1);
     int tin;
-    const uint32_t sg = seg_of(j * a.gk, tin);  // per lane in a paged cache
+    const uint32_t sg = seg_of_lane(j * a.gk, tin);
     const uint32_t jg = paged ? (uint32_t)(tin >> a.pm.gk_shift) : (uint32_t)j;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
