@@ -121,12 +121,12 @@ def test_release_reuses_pages_and_pool_capacity():
     assert row_rel_err(out[1], c.oracle_out(1)).max() <= ATTN_TOL
 
 
-def test_chunk_attention_over_pages():
+@pytest.mark.parametrize("n_q", [24, 7])   # 8-row groups; 4-row groups (odd n_q)
+def test_chunk_attention_over_pages(n_q):
     from paper_2607_16248_amd import kvq
     w = W("chunk_paged", 2, 32, 8, (1200, 777), 1, 1)
     c = Case(w, page_tokens=64)
     c.append_all([100, 1100])
-    n_q = 24
     q = np.stack([gen_q_chunk(w, n_q, 0, s) for s in range(w.batch)])
     out = torch.empty((2, n_q, 32, 128), dtype=torch.float32, device="cuda")
     ws = torch.empty(kvq.kvq_chunk_workspace_bytes(c.cache.handle, n_q), dtype=torch.uint8, device="cuda")
@@ -135,3 +135,32 @@ def test_chunk_attention_over_pages():
     for s in range(2):
         ref = oracle.chunk_seq(q[s], c.K[s], c.V[s], 1, 1, 32, 32, 0)
         assert row_rel_err(got[s], ref).max() <= ATTN_TOL, s
+
+
+def test_append_decode_steps_on_pages():
+    """Token-by-token kvq_append_decode over a paged and a contiguous cache:
+    70 steps cross two key-group flushes (pages taken mid-stream); outputs
+    bit-identical at every step, bytes equal to the oracle at the end."""
+    from paper_2607_16248_amd import kvq
+    w = W("steps_paged", 2, 32, 8, (400, 400), 1, 1)
+    paged, flat = Case(w, page_tokens=64), Case(w)
+    for c in (paged, flat):
+        K = np.stack([c.K[s][:300] for s in range(2)])
+        V = np.stack([c.V[s][:300] for s in range(2)])
+        c.cache.append(torch.from_numpy(K).cuda(), torch.from_numpy(V).cuda(), [300, 300])
+    q = torch.from_numpy(np.stack(paged.q)).cuda()
+    for t in range(300, 370):
+        outs = []
+        for c in (paged, flat):
+            Kn = torch.from_numpy(np.stack([c.K[s][t:t + 1] for s in range(2)])).cuda()
+            Vn = torch.from_numpy(np.stack([c.V[s][t:t + 1] for s in range(2)])).cuda()
+            o = torch.empty((2, 32, 128), dtype=torch.float32, device="cuda")
+            kvq.kvq_append_decode(c.cache.handle, Kn, Vn, [1, 1], q, o, c.cache.workspace())
+            outs.append(o)
+        torch.cuda.synchronize()
+        assert torch.equal(outs[0], outs[1]), t
+    paged.cache.check()
+    for s in range(2):
+        for h in (0, 3):
+            ref = oracle.build_head(paged.K[s][:370, h, :], paged.V[s][:370, h, :], 1, 1, 32, 32, 0)
+            assert (paged.cache.export(s, h) == ref).all(), (s, h)
