@@ -1,6 +1,7 @@
 /*
- * kvq — packed low-bit KV cache and single-token decode attention for
- * AMD Instinct MI355X (gfx950).  Plain C ABI.
+ * kvq — packed low-bit KV cache and attention over it for AMD Instinct
+ * MI355X (gfx950): single-token decode, chunk queries (the last n_q tokens,
+ * causal) and a paged layout for serving.  Plain C ABI.
  *
  * The computation is attention over a persistent low-bit KV cache.  The
  * paper evaluates KbVb caches, b-bit keys and b-bit values with

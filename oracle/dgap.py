@@ -19,7 +19,7 @@ What the paper fixes (Methodology):
 - Ablation, "Effect of risk threshold": tau = 0.60; "Detector-corrector
   architecture": MLP detector and corrector.
 
-Readings where the paper is silent (each listed in the design doc):
+Readings where the paper is silent:
 - TopK orders by logit, descending, ties by lower vocabulary index.
 - phi has 12 entries (see ``features``); xi has 5 per candidate.
 - f_theta and g_psi are one-hidden-layer ReLU MLPs; g_psi is shared by all
