@@ -160,11 +160,23 @@ __device__ __forceinline__ Work find_work(const DecodeArgs& a) {
   int si = 0;
   for (int i = 1; i < a.nseq; ++i) si = (a.seq[i].wg_begin <= wg) ? i : si;
   const int local = wg - a.seq[si].wg_begin;
-  const int hv = local / a.seq[si].nsplit;
-  Work w{si, hv, 0, local % a.seq[si].nsplit};
+  const int ns = a.seq[si].nsplit;
+  const int hv = local / ns;
+  Work w{si, hv, 0, local % ns};
   if (CHUNK && a.nrg > 1) {  // chunk queries: kv head and row group
-    w.h = hv / a.nrg;
-    w.rg = hv - w.h * a.nrg;
+    const int units = a.hkv * ns;  // (kv head, split) pairs
+    if (units % 8 == 0) {
+      // Row groups of one (kv head, split) unit read the same tokens: give
+      // them workgroup ids 8 apart, so that they land on one XCD (ids go
+      // round-robin over the 8) and their re-reads hit its L2.
+      const int q = local >> 3, u = ((q / a.nrg) << 3) + (local & 7);
+      w.rg = q % a.nrg;
+      w.h = u / ns;
+      w.sp = u % ns;
+    } else {
+      w.h = hv / a.nrg;
+      w.rg = hv - w.h * a.nrg;
+    }
   }
   return w;
 }

@@ -189,6 +189,14 @@ int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int n
   // wait for a free slot would add a whole split's time to the launch.
   const int64_t target = std::max<int64_t>(target_workgroups(occ) - tails, target_workgroups(occ) / 2);
   int64_t st = (total + target - 1) / target;
+  if (nrg > 1 && !seqs.empty()) {
+    // chunk queries: every row group of a (kv head, split) unit reads the
+    // unit's tokens; units of at most ~1 MiB let the row groups that share
+    // an XCD find them in its L2 (more workgroup rounds instead)
+    const int i0 = seqs[0];
+    const int64_t tok_bytes = 16 * (c->bk[i0] + c->bv[i0]) + 512 / gk + 4 * (kvq::kHeadDim / c->d.value_group);
+    st = std::min<int64_t>(st, ((int64_t)1 << 20) / tok_bytes);
+  }
   st = std::max<int64_t>(st, (lq_max + kMaxSplits - 1) / kMaxSplits);
   st = (st + gk - 1) / gk * gk;
   st = std::max<int64_t>(st, (int64_t)gk * kMinGroupsPerSplit);
