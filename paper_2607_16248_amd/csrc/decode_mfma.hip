@@ -628,7 +628,7 @@ decode_mfma_kernel(DecodeArgs a) {
       // score lanes of row H / HPL, as their element H % HPL
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
-        const int H = 4 * q + hc;
+        const int H = (GQ == 5 && q == 1) ? 4 : 4 * q + hc;  // five heads: quad 1 is head 4 alone
         float av;
         if constexpr (HPL == 1) {
           av = __shfl(alpha[0], 16 * H);
@@ -663,8 +663,13 @@ decode_mfma_kernel(DecodeArgs a) {
     wave_lds_sync();
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[(4 * q + hc) * kPRow + 4 * row]);
-      const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[(4 * q + hc) * kPRow + 16 + 4 * row]);
+      // Five heads: the second quad carries head 4 alone, with the hi and
+      // lo halves of its P' in columns 0-3 and 4-7 of one MFMA (columns
+      // 8-15 zero) instead of two MFMAs over an almost empty quad.
+      const bool solo = GQ == 5 && q == 1;
+      const int Hp = solo ? 4 : 4 * q + hc;
+      const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[Hp * kPRow + 4 * row]);
+      const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[Hp * kPRow + 16 + 4 * row]);
       const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
 
       // P' = p * s_v as fp16 hi + lo: the product and its residual are each
@@ -681,31 +686,29 @@ decode_mfma_kernel(DecodeArgs a) {
         float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
         float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
         keep_f32(g0, g1);
-        bhi[t] = hw;
-        blo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
+        const uint32_t lw = h2u((h2_t){(_Float16)g0, (_Float16)g1});
+        bhi[t] = solo ? (hc == 0 ? hw : hc == 1 ? lw : 0u) : hw;
+        blo[t] = lw;
         const h2_t z2 = u2h(cur.zv[t]);
         zacc[q] = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc[q]));
       }
       const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) {
+        h8_t av;
         if constexpr (BV == 1) {
           const uint32_t byte = (cur.vx[mb >> 2] >> (8 * (mb & 3))) & 0xFFu;
-          const h8_t av = *reinterpret_cast<const h8_t*>(&vtab[byte * 4]);
-          acc[q][mb] = mfma(av, BH, acc[q][mb]);
-          acc[q][mb] = mfma(av, BL, acc[q][mb]);
+          av = *reinterpret_cast<const h8_t*>(&vtab[byte * 4]);
         } else if constexpr (BV == 2) {
           const uint32_t x = cur.vx[mb >> 1] >> (16 * (mb & 1));
           const uint2 t0 = *reinterpret_cast<const uint2*>(&vtab[(x & 0xFFu) * 2]);
           const uint2 t1 = *reinterpret_cast<const uint2*>(&vtab[((x >> 8) & 0xFFu) * 2]);
-          const h8_t av = __builtin_bit_cast(h8_t, (u4_t){t0.x, t0.y, t1.x, t1.y});
-          acc[q][mb] = mfma(av, BH, acc[q][mb]);
-          acc[q][mb] = mfma(av, BL, acc[q][mb]);
+          av = __builtin_bit_cast(h8_t, (u4_t){t0.x, t0.y, t1.x, t1.y});
         } else {
-          const h8_t av = whole8<BV>(&cur.vx[(BV / 4) * mb]);
-          acc[q][mb] = mfma(av, BH, acc[q][mb]);
-          acc[q][mb] = mfma(av, BL, acc[q][mb]);
+          av = whole8<BV>(&cur.vx[(BV / 4) * mb]);
         }
+        acc[q][mb] = mfma(av, BH, acc[q][mb]);
+        if (!solo) acc[q][mb] = mfma(av, BL, acc[q][mb]);
       }
     }
   };
@@ -769,13 +772,19 @@ decode_mfma_kernel(DecodeArgs a) {
     float zs = zacc[q];
     zs += __shfl_xor(zs, 16);
     zs += __shfl_xor(zs, 32);
-    const int H = 4 * q + ehc;
+    const bool solo = GQ == 5 && q == 1;  // head 4: hi columns 0-3, lo columns 4-7
+    const int H = solo ? 4 : 4 * q + ehc;
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
-      if (H < GQ && exc == (16 * mb) / a.gv) {
+      f4_t v = acc[q][mb];
+      if (solo) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] += __shfl_xor(v[e], 4);
+      }
+      if ((solo ? ehc == 0 : H < GQ) && exc == (16 * mb) / a.gv) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + e] = acc[q][mb][e] * kAccScale + zs;
+          red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + e] = v[e] * kAccScale + zs;
       }
     }
   }
