@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_FP16_PEAK_TFLOPS = 2500.0  # dense fp16 / bf16 matrix cores
 METRIC = "decode-attn effective KV GB/s (% of HBM peak) + µs/layer, K1V1 @128K ctx"
 
 
@@ -209,6 +210,9 @@ def chunk_leg(handles, w, launch_bytes: int, stream, iters: int):
         del q, o, ws
     out["note"] = ("each row group of up to 8 (query, head) rows is one pass over the kv head's cache; "
                    "the useful flops count each visible (query, head, token) once")
+    # the matrix-core roofline of the contraction (fp16 operands, fp32 accumulation)
+    out["roofline"] = {"bound": "mfma", "peak": MFMA_FP16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                       "frac": [round(t / MFMA_FP16_PEAK_TFLOPS, 4) for t in out["useful_tflops"]]}
     return out
 
 
@@ -264,6 +268,10 @@ def paged_leg(w, qs, dev, stream, iters: int, nlayers: int = 8):
         torch.cuda.synchronize()
         outs[name] = o
     out["outputs_bit_identical"] = bool(torch.equal(outs["contiguous"], outs["paged"]))
+    nbytes = sum(packed_bytes(L, w, bk, bv) for L, bk, bv in zip(w.lens, w.bits_k, w.bits_v))
+    out["roofline_paged"] = {"bound": "hbm", "achieved": round(nbytes / (out["split_us_paged"] * 1e-6) / 1e9, 2),
+                             "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                             "frac": round(nbytes / (out["split_us_paged"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
     return out
 
 
