@@ -92,7 +92,7 @@ __device__ __forceinline__ void pack_value_blocks_matrix(const uint8_t* codes, i
 }
 
 __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, int gi, int bk,
-                               int bv, uint8_t* codes) {
+                               int bv, uint8_t* codes, uint32_t* vmax) {
   uint8_t* blk = a.arena + S.head0 + (uint64_t)h * a.head_stride;  // the fp16 ring's region
   const int gk = a.gk, j = S.Lq_old / gk + gi, p0 = j * gk;
   const int c = threadIdx.x;
@@ -132,7 +132,10 @@ __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, i
     pack_rows(codes, gk, bk, seg + a.kc + (size_t)t0 * 16 * bk);
   __syncthreads();
 
-  // values: one item per (token, value group)
+  // values: one item per (token, value group); the largest value scale of
+  // the group raises the head's bound (decode sizes its weight shift by it)
+  if (threadIdx.x == 0) *vmax = 0u;
+  __syncthreads();
   const int ng = kHeadDim / a.gv;
   for (int it = threadIdx.x; it < gk * ng; it += blockDim.x) {
     const int i = it / ng, g = it % ng;
@@ -149,6 +152,7 @@ __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, i
     uint16_t sb = 0;
     const bool ok = finite && half_ceil((mx - mn) / (double)((1 << bv) - 1), sb);
     if (!ok) { raise_range(a.arena); sb = 0x7E00; }
+    else atomicMax(vmax, (uint32_t)sb);  // positive fp16 patterns order like their values
     const double sv = half_bits_to_double(sb);
     for (int e = 0; e < a.gv; ++e) {
       const double v = half_bits_to_double(row[e]);
@@ -165,6 +169,7 @@ __device__ void quantize_group(const AppendArgs& a, const AppendSeq& S, int h, i
     }
   }
   __syncthreads();
+  if (threadIdx.x == 0) atomicMax(reinterpret_cast<uint32_t*>(blk + a.vb), *vmax);
   if (a.matrix)
     pack_value_blocks_matrix(codes, gk, bv, seg + a.vc + (size_t)t0 * 16 * bv);
   else
@@ -187,6 +192,7 @@ __device__ void copy_ring(const AppendArgs& a, const AppendSeq& S, int h) {
 
 __global__ __launch_bounds__(128) void append_kernel(AppendArgs a, int bk, int bv) {
   __shared__ uint8_t codes[128 * kHeadDim];
+  __shared__ uint32_t vmax;
   const int wg = blockIdx.x;
   int si = 0;
   for (int i = 1; i < a.nseq; ++i) si = (a.seq[i].wg_begin <= wg) ? i : si;
@@ -194,7 +200,7 @@ __global__ __launch_bounds__(128) void append_kernel(AppendArgs a, int bk, int b
   const int local = wg - S.wg_begin;
   const int nquant = a.quantize ? S.n_quant * a.hkv : 0;
   if (local < nquant) {
-    quantize_group(a, S, local / S.n_quant, local % S.n_quant, bk, bv, codes);
+    quantize_group(a, S, local / S.n_quant, local % S.n_quant, bk, bv, codes, &vmax);
   } else if (S.do_copy) {
     copy_ring(a, S, local - nquant);
   }
@@ -202,6 +208,10 @@ __global__ __launch_bounds__(128) void append_kernel(AppendArgs a, int bk, int b
 
 __global__ __launch_bounds__(256) void table_set_kernel(TableSet t) {
   for (int i = threadIdx.x; i < t.n; i += blockDim.x) t.table[t.idx[i]] = t.val[i];
+}
+
+__global__ __launch_bounds__(256) void word_reset_kernel(WordReset r) {
+  for (int i = threadIdx.x; i < r.n; i += blockDim.x) *reinterpret_cast<uint32_t*>(r.arena + r.off[i]) = 0u;
 }
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, size_t n) {
@@ -220,6 +230,12 @@ int launch_append(const AppendArgs& a, int bk, int bv, void* stream) {
 int launch_table_set(const TableSet& t, void* stream) {
   if (t.n <= 0) return 0;
   hipLaunchKernelGGL(table_set_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t);
+  return (int)hipGetLastError();
+}
+
+int launch_word_reset(const WordReset& r, void* stream) {
+  if (r.n <= 0) return 0;
+  hipLaunchKernelGGL(word_reset_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, r);
   return (int)hipGetLastError();
 }
 

@@ -134,15 +134,15 @@ __device__ __forceinline__ h8_t whole8(const uint32_t* x) {
   return __builtin_bit_cast(h8_t, w);
 }
 
-// Weights p reach up to 2^S (S = PShift) instead of 1 so that p * s_v, a
-// B operand in fp16 hi + lo halves, keeps its lo half out of the subnormal
-// range: with 4- and 8-bit values s_v is small (range / 15 or / 255).  S is
-// the largest shift with p * s_v < 65504 for every valid scale (s_v <= 514
-// at 8 bits, 8736 at 4 bits; p <= 1 before the shift).
-template <int B>
-struct PShift {
-  static constexpr int value = B == 8 ? 6 : B == 4 ? 2 : 0;
-};
+// Weights p reach up to 2^S instead of 1 so that p * s_v, a B operand in
+// fp16 hi + lo halves, stays clear of the fp16 subnormal range, where it
+// would lose its low bits (small value scales: few-bit codes of values with
+// a small range, or 4- and 8-bit codes, whose scale is range / 15 or / 255).
+// S is chosen per (sequence, kv head) from the bound the append kernel keeps
+// on the head's value scales: 2^S * bound < 2^15 (p <= 1 before the shift).
+// Every split record carries its own reference, so the merge needs no
+// common S.
+constexpr int kMaxPShift = 30;
 
 // log2 of one code unit in a key operand (the lowest element pair sits at
 // mantissa bit 6 at 1 and 2 bits, whole codes at bits 4.. and 0..), and in a
@@ -296,7 +296,6 @@ decode_mfma_kernel(DecodeArgs a) {
   constexpr int NQ = NH / 4;                  // head quads in the value columns
   constexpr int RS = 16 / NH;                 // score rows per head
   constexpr int kDzRows = (kChunk * NH + kQRow - 1) / kQRow;
-  constexpr int kPShift = PShift<BV>::value;
   // per wave: Q' hi rows, lo rows, q~ rows, then the zero-point terms of up
   // to kChunk key groups (16-byte aligned: rows are read with 16-byte loads)
   __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * NH + kDzRows) * kQRow];
@@ -428,6 +427,9 @@ decode_mfma_kernel(DecodeArgs a) {
   constexpr int kStages = MatrixStages<BK, BV, BPG, GQ>::value;
   BlockData<BK, BV> b0, b1, b2;
   h8_t zq[4];
+  // the bound on this head's value scales, issued with the first block's
+  // loads so that its latency hides behind theirs
+  const uint32_t vbound = *reinterpret_cast<const uint32_t*>(blk + a.vb);
   if (nblocks > 0) {
     load(0, b0);
     if constexpr (kStages == 3) load(min(1, last), b1);
@@ -510,6 +512,20 @@ decode_mfma_kernel(DecodeArgs a) {
     }
   };
   if (nblocks > 0) fill_table(0, zq);
+
+  // the weight shift of this (sequence, kv head): the largest S <= 30 with
+  // 2^S * bound < 2^15 (bound = the largest value scale packed so far)
+  float pshift = (float)kMaxPShift;
+  {
+    const uint32_t vbits = vbound & 0xFFFFu;
+    if (vbits >= 0x7C00u) {
+      pshift = 0.f;
+    } else if (vbits != 0u) {
+      int ex = 0;
+      frexpf(h2f(vbits), &ex);  // bound < 2^ex
+      pshift = (float)min(kMaxPShift, max(0, 15 - ex));
+    }
+  }
 
   // Score layout: m[hh] = the softmax reference of head HPL*row + hh
   // (uniform over the row), l[hh] = the sum of the lane's own weights.
@@ -597,15 +613,15 @@ decode_mfma_kernel(DecodeArgs a) {
     // (and its exponential) is skipped while later scores stay under the
     // reference.  Each lane compares its own two scores; only a block with a
     // score above its reference reduces the maxima across the row's lanes.
-    // With a weight shift (PShift) m and every score are kept kPShift lower,
-    // so the weights reach 2^kPShift; m is the reference of the record.
+    // With the weight shift m and every score are kept pshift lower, so the
+    // weights reach 2^pshift; m is the reference of the record.
     const float ninf = -__builtin_inff();
     float bm[HPL];
     bool up = false;
 #pragma unroll
     for (int hh = 0; hh < HPL; ++hh) {
       const float b = fmaxf(raw[hh][0], raw[hh][1]);
-      bm[hh] = kPShift ? fmaf(b, cs[hh], -(float)kPShift) : b * cs[hh];
+      bm[hh] = fmaf(b, cs[hh], -pshift);
       up |= bm[hh] > m[hh];
     }
     if (__builtin_amdgcn_ballot_w64(up)) {

@@ -148,11 +148,12 @@ PagedArena paged_arena(const kvq_cache_desc* d) {
   PagedArena A;
   const int bk = d->bits_k[0], bv = d->bits_v[0], P = d->page_tokens;
   const int64_t W = (int64_t)d->fp16_window + d->key_group;
-  A.page = kvq::head_layout(bk, bv, P, d->key_group, d->value_group, 0);
+  A.page = kvq::head_layout(bk, bv, P, d->key_group, d->value_group, 0, false);
   A.ring = kvq::head_layout(bk, bv, 0, d->key_group, d->value_group, W);
   A.seq_lay = A.page;
   A.seq_lay.tk = A.ring.tk;
   A.seq_lay.tv = A.ring.tv;
+  A.seq_lay.vb = A.ring.vb;
   A.seq_lay.stride = A.ring.stride;
   A.max_pages = (int32_t)((packed_capacity(d) + P - 1) / P);
   A.num_pages = d->num_pages > 0 ? d->num_pages : d->batch * A.max_pages;
@@ -383,6 +384,25 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int32_t n_max,
   if (c->paged && pages_needed > (int64_t)c->free_pages.size())
     return fail(KVQ_ERR_CAPACITY, "the append needs %lld more pages, the pool has %zu free", (long long)pages_needed,
                 c->free_pages.size());
+  {
+    // a sequence's first packed group starts a fresh bound on its value
+    // scales (after kvq_seq_release or kvq_cache_reset the old one is stale)
+    kvq::WordReset r{};
+    r.arena = c->arena;
+    for (int i = 0; i < d.batch; ++i) {
+      if (c->Lq[i] != 0 || Lq_new[i] == 0) continue;
+      for (int h = 0; h < d.num_kv_heads; ++h) {
+        r.off[r.n++] = c->head0[i] + (uint64_t)h * c->lay[i].stride + c->lay[i].vb;
+        if (r.n == kvq::kTableSetMax) {
+          const int e = kvq::launch_word_reset(r, stream);
+          if (e) return hip_fail(e, "bound reset launch");
+          r.n = 0;
+        }
+      }
+    }
+    const int e = kvq::launch_word_reset(r, stream);
+    if (e) return hip_fail(e, "bound reset launch");
+  }
   if (c->paged && pages_needed > 0) {
     // take the pages and write their block-table entries (ordered before the append launch)
     kvq::TableSet t{};
@@ -420,7 +440,7 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int32_t n_max,
       a.V = static_cast<const uint16_t*>(V);
       a.head_stride = lay.stride;
       a.kc = (uint32_t)lay.kc; a.km = (uint32_t)lay.km; a.vc = (uint32_t)lay.vc;
-      a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
+      a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv; a.vb = (uint32_t)lay.vb;
       a.n_max = n_max; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
       a.quantize = quant ? 1 : 0;
       a.matrix = c->matrix[cls.second[0]];
@@ -552,7 +572,7 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.ws = static_cast<float*>(ws);
     a.head_stride = lay.stride;
     a.kc = (uint32_t)lay.kc; a.km = (uint32_t)lay.km; a.vc = (uint32_t)lay.vc;
-    a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv;
+    a.vm = (uint32_t)lay.vm; a.tk = (uint32_t)lay.tk; a.tv = (uint32_t)lay.tv; a.vb = (uint32_t)lay.vb;
     a.hq = d.num_q_heads; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
     a.split_tokens = p.st[cls.second[0]];
     a.qscale = qscale;

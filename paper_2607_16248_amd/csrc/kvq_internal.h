@@ -32,10 +32,11 @@ inline uint64_t align_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
 
 struct HeadLayout {
   uint64_t kc, km, vc, vm, tk, tv;  // byte offsets inside a (seq, head) block
+  uint64_t vb;                      // bound on the value scales packed so far (fp16 bits, in a uint32)
   uint64_t stride;                  // block size
 };
 
-inline HeadLayout head_layout(int bk, int bv, int64_t cq, int gk, int gv, int64_t w) {
+inline HeadLayout head_layout(int bk, int bv, int64_t cq, int gk, int gv, int64_t w, bool with_bound = true) {
   HeadLayout L{};
   uint64_t o = 0;
   L.kc = o; o = align_up(o + (uint64_t)cq * 16 * bk, kAlign);
@@ -44,6 +45,7 @@ inline HeadLayout head_layout(int bk, int bv, int64_t cq, int gk, int gv, int64_
   L.vm = o; o = align_up(o + (uint64_t)cq * (kHeadDim / gv) * 4, kAlign);
   L.tk = o; o = align_up(o + (uint64_t)w * kHeadDim * 2, kAlign);
   L.tv = o; o = align_up(o + (uint64_t)w * kHeadDim * 2, kAlign);
+  L.vb = o; o = with_bound ? align_up(o + 4, kAlign) : o;
   L.stride = o;
   return L;
 }
@@ -111,7 +113,7 @@ struct AppendArgs {
   const uint16_t* K;  // fp16 [batch][n_max][Hkv][128]
   const uint16_t* V;
   uint64_t head_stride;
-  uint32_t kc, km, vc, vm, tk, tv;
+  uint32_t kc, km, vc, vm, tk, tv, vb;
   int32_t n_max, hkv, gk, gv, W, nseq, total_wg;
   int32_t quantize;   // 1: pack groups in this launch
   int32_t matrix;     // 1: matrix layout (kvq_layout.h) for this bit class
@@ -150,7 +152,7 @@ struct DecodeArgs {
   const uint16_t* V_new;
   int32_t n_max, pad;
   uint64_t head_stride;
-  uint32_t kc, km, vc, vm, tk, tv;
+  uint32_t kc, km, vc, vm, tk, tv, vb;
   int32_t hq, hkv, gk, gv, W, split_tokens, nseq, total_wg;
   float qscale;       // log2(e) / sqrt(d)
   DecodeSeq seq[kMaxSeqPerLaunch];
@@ -230,6 +232,13 @@ struct ExportArgs {
 // Launchers (defined next to their kernels).  Return a hipError_t as int.
 int launch_append(const AppendArgs& a, int bk, int bv, void* stream);
 int launch_table_set(const TableSet& t, void* stream);
+// Zero the given 32-bit words of the arena (byte offsets), up to kTableSetMax per launch.
+struct WordReset {
+  uint8_t* arena;
+  int32_t n, pad;
+  uint64_t off[kTableSetMax];
+};
+int launch_word_reset(const WordReset& r, void* stream);
 int launch_decode(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
 int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stream);
 // Matrix-core decode (and the matrix layout) for this bit class: 4, 5 or 8

@@ -47,7 +47,7 @@ def expected_bytes(batch, hkv, max_tokens, gk, gv, R, bits_k, bits_v):
     total = 256
     for bk, bv in zip(bits_k, bits_v):
         per_head = (align(cq * 16 * bk) + align(cq // gk * 512) + align(cq * 16 * bv)
-                    + align(cq * (128 // gv) * 4) + 2 * align(W * 256))
+                    + align(cq * (128 // gv) * 4) + 2 * align(W * 256) + align(4))  # + value-scale bound
         total += hkv * per_head
     return total
 
