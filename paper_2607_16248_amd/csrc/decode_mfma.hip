@@ -311,6 +311,13 @@ decode_mfma_kernel(DecodeArgs a) {
   const uint8_t* blk = a.arena + S.head0 + (uint64_t)wk.h * a.head_stride;
   // wave index as a scalar so that per-wave loop bounds stay in SGPRs
   const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  // The bound on this head's value scales (it sets the weight shift below).
+  // Issued first as a vector load, held there by the compiler barrier, and
+  // consumed after the query is prepared, so its latency hides behind the
+  // first blocks' loads (a scalar load would be waited for with the loads of
+  // the arguments, before those go out).
+  uint32_t vbound = __builtin_amdgcn_raw_buffer_load_b32(head_rsrc(blk + a.vb, 4), 0, 0, 0);
+  asm volatile("" ::: "memory");
 
   if constexpr (BV == 1) {
     for (int i = threadIdx.x; i < 256 * 4; i += blockDim.x) {
@@ -427,9 +434,6 @@ decode_mfma_kernel(DecodeArgs a) {
   constexpr int kStages = MatrixStages<BK, BV, BPG, GQ>::value;
   BlockData<BK, BV> b0, b1, b2;
   h8_t zq[4];
-  // the bound on this head's value scales, issued with the first block's
-  // loads so that its latency hides behind theirs
-  const uint32_t vbound = *reinterpret_cast<const uint32_t*>(blk + a.vb);
   if (nblocks > 0) {
     load(0, b0);
     if constexpr (kStages == 3) load(min(1, last), b1);
@@ -517,6 +521,7 @@ decode_mfma_kernel(DecodeArgs a) {
   // 2^S * bound < 2^15 (bound = the largest value scale packed so far)
   float pshift = (float)kMaxPShift;
   {
+    asm volatile("" : "+v"(vbound));
     const uint32_t vbits = vbound & 0xFFFFu;
     if (vbits >= 0x7C00u) {
       pshift = 0.f;
