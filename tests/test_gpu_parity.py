@@ -277,3 +277,28 @@ def test_small_value_scales(bits, scale):
     err = row_rel_err(out[0], c.oracle_out(0)).max()
     log(f"[parity] value scale {scale:g}, K{bits}V{bits}: max row-relative error {err:.3e}")
     assert err <= ATTN_TOL
+
+
+@pytest.mark.parametrize("how", ["reset", "release"])
+def test_value_bound_starts_fresh(how):
+    # A sequence packed with values of scale ~1e4 (a value-scale bound near
+    # 2^15: no weight shift), then emptied and refilled with values of scale
+    # ~1e-5: the refill must start a fresh bound, since with the stale one the
+    # shift stays 0 and p * s_v of the small values (value scales ~1e-4) is
+    # below the fp16 normal range.
+    w = W("vbound_fresh_k1", 1, 32, 8, 3000, 1, 1, R=5, cfg=96)
+    kw = {"page_tokens": 256, "num_pages": 16} if how == "release" else {}
+    c = Case(w, **kw)
+    V0 = c.V
+    c.V = [(v.astype(np.float32) * 3000.0).astype(np.float16) for v in V0]
+    c.append_all()
+    if how == "reset":
+        c.cache.reset()
+    else:
+        c.cache.release(0)
+    c.V = [(v.astype(np.float32) * 1e-5).astype(np.float16) for v in V0]
+    c.append_all()
+    out = c.decode()
+    err = row_rel_err(out[0], c.oracle_out(0)).max()
+    log(f"[parity] value bound after {how}: max row-relative error {err:.3e}")
+    assert err <= ATTN_TOL
