@@ -10,6 +10,8 @@ seeded, byte-identical cache, through the C ABI.
   queries per group), vector kernel with 1, 2, 4 or 8 rows;
 - n_q = 1 equals kvq_decode_attention bit for bit; results are bitwise
   reproducible.
+- value scales of ~1e-5 (the weight shift from the head's value-scale
+  bound), on contiguous and paged caches.
 """
 import numpy as np
 import pytest
@@ -116,3 +118,18 @@ def test_long_context_chunk_sampled_heads(n_q, bits):
     q, out = _chunk(c, n_q)
     worst = _check(c, q, out, heads=heads)
     log(f"[chunk] {w.name} n_q={n_q}: max row-relative error {worst:.3e}")
+
+
+@pytest.mark.parametrize("bits,paged", [(1, False), (2, True), (8, False)])
+def test_chunk_small_value_scales(bits, paged):
+    # values of scale ~1e-5: the causal kernels take the same per-head weight
+    # shift as single-token decode, sized by the head's bound on the packed
+    # value scales (contiguous and paged caches)
+    w = W(f"chunk_vscale_k{bits}", 2, 32, 8, (700, 1300), bits, bits, R=0, cfg=97)
+    kw = {"page_tokens": 256, "num_pages": 16} if paged else {}
+    c = Case(w, **kw)
+    c.V = [(v.astype(np.float32) * 1e-5).astype(np.float16) for v in c.V]
+    c.append_all()
+    q, out = _chunk(c, 16)
+    worst = _check(c, q, out)
+    log(f"[chunk] value scale 1e-5, K{bits}V{bits}, paged={paged}: max row-relative error {worst:.3e}")
