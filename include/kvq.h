@@ -114,7 +114,11 @@ kvq_status kvq_seq_release(kvq_cache* cache, int32_t seq);
 int64_t kvq_free_pages(const kvq_cache* cache);
 
 /* Append tokens and quantize every key group that leaves the fp16 window
- * (the fused quantize-on-append step).
+ * (the fused quantize-on-append step).  Defines the b-bit key and value
+ * storage of a KbVb cache (Motivation, "Accuracy Loss under Aggressive KV
+ * Quantization", Methodology paragraph), with the asymmetric min-max rule
+ * stated at the top of this header (Related Work, "KV-cache quantization and
+ * distribution preservation": asymmetric key/value formats).
  *   K, V : device fp16 [batch][n_max][Hkv][d]; sequence i appends rows
  *          0 .. n_new[i]-1 of its slice.  Read only.
  *   n_new: host int32 [batch], 0 <= n_new[i] <= n_max.
@@ -131,7 +135,10 @@ kvq_status kvq_append(kvq_cache* cache, const void* K, const void* V, int32_t n_
  * max_tokens under the current split setting. */
 size_t kvq_workspace_bytes(const kvq_cache* cache);
 
-/* Single-token decode attention over every cached token of every sequence:
+/* Single-token decode attention over every cached token of every sequence,
+ * the decoder's scaled dot-product attention softmax(Q K^T / sqrt(d_k)) V
+ * (Introduction) at one query per sequence per step (Experimental Setup,
+ * Testbed: batch-1 decoding):
  *   out[i][h][:] = softmax(q[i][h] . K^[i][kv(h)]^T / sqrt(d)) V^[i][kv(h)]
  * with kv(h) = h / (Hq / Hkv), K^ and V^ the dequantized cache (fp16 tail
  * tokens exact).  q: device fp16 [batch][Hq][d], finite (a NaN or infinity
@@ -207,7 +214,12 @@ kvq_status kvq_chunk_attention(const kvq_cache* cache, const void* q, int32_t n_
 /* Dequantize tokens [tok0, tok0 + ntok) of one sequence into device fp32
  * K_out, V_out [ntok][Hkv][d]: fmaf(code, s, z) for packed tokens (the
  * exact z + code*s rounded once to fp32) and the fp16 value for tail
- * tokens.  For checking; not on the decode path. */
+ * tokens.  These are the dequantized keys and values K^, V^ that decode
+ * attends over (the KbVb cache of Motivation, "Accuracy Loss under
+ * Aggressive KV Quantization", read back through the rule at the top of
+ * this header).  For checking; not on the decode path.  Errors:
+ * KVQ_ERR_ARG (seq out of range, a token range outside [0, L), null
+ * outputs), KVQ_ERR_HIP. */
 kvq_status kvq_dequant(const kvq_cache* cache, int32_t seq, int32_t tok0, int32_t ntok,
                        float* K_out, float* V_out, void* stream);
 
@@ -221,7 +233,12 @@ kvq_status kvq_dequant(const kvq_cache* cache, int32_t seq, int32_t tok0, int32_
 size_t kvq_export_bytes(const kvq_cache* cache, int32_t seq, int32_t kv_head);
 
 /* Copy the canonical image of (seq, kv_head) into device memory `dst` of
- * `bytes` >= kvq_export_bytes(...).  Device-to-device copies on `stream`. */
+ * `bytes` >= kvq_export_bytes(...): the persistent low-bit cache the paper
+ * keeps unchanged across decode steps (Methodology, "DGAP Overview", online
+ * restoration framework), in the byte order above, for checking and for
+ * saving a cache.  Device-to-device copies and a reorder kernel on
+ * `stream`.  Errors: KVQ_ERR_ARG (seq or kv_head out of range, null dst),
+ * KVQ_ERR_CAPACITY (bytes too small), KVQ_ERR_HIP. */
 kvq_status kvq_export(const kvq_cache* cache, int32_t seq, int32_t kv_head, void* dst,
                       size_t bytes, void* stream);
 

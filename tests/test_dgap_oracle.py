@@ -125,3 +125,58 @@ def test_permutation_equivariance():
     assert a.corrected and b.corrected
     assert np.allclose(b.logits, a.logits[perm], rtol=0, atol=1e-12)
     assert np.array_equal(perm[b.idx], a.idx)
+
+
+def test_top8_mass_in_closed_form():
+    # 12 logits at log 2 and 20 at 0: the top 8 hold 8 * 2 / (12 * 2 + 20) of
+    # the mass, the top 16 hold (12 * 2 + 4) / 44 (a 7- or 9-entry slice, or
+    # the top-k slice, gives another number)
+    z = np.concatenate([np.full(12, np.log(2.0)), np.zeros(20)])
+    phi = dgap.features(z, 16)
+    assert abs(phi[4] - 16 / 44) <= 1e-15
+    assert abs(phi[3] - 28 / 44) <= 1e-15
+    phi8 = dgap.features(z, 8)
+    assert abs(phi8[4] - 16 / 44) <= 1e-15 and abs(phi8[3] - 16 / 44) <= 1e-15
+
+
+def test_smallest_gap_spans_exactly_the_top_eight():
+    # leading logits with gaps 1, 1.5, 1, 1.5, 0.8, 1.2, 0.25 between v1..v8,
+    # then 0.0625 between v8 and v9: the smallest of the 7 gaps is 0.25; six
+    # gaps would give 0.8 and eight 0.0625
+    v = np.array([10.0, 9.0, 7.5, 6.5, 5.0, 4.25, 3.0, 2.75, 2.6875])
+    z = np.concatenate([v, np.full(23, -4.0)])
+    for k in (8, 9, 16):
+        assert dgap.features(z, k)[9] == 0.25
+    phi = dgap.features(z, 9)
+    assert phi[6] == 1.0 and phi[7] == 1.5 and phi[8] == (10.0 - 2.6875) / 8
+
+
+def test_corrector_by_hand_with_candidate_and_shape_inputs():
+    # The 10-logit row of test_candidate_features_by_hand, k = 8: xi is known by
+    # hand, and so are phi_6 = v1 - v2 = 0, phi_7 = v2 - v3 = 0.5 and
+    # phi_8 = (v1 - v8) / 7 = 0.5.  The corrector input is [xi_k (5), phi (12)],
+    # so phi_j sits in row 5 + j of C1.
+    z = np.array([1.0, 4.0, 2.0, 4.0, 0.5, 3.0, -1.0, 2.5, 0.0, 3.5])
+    v = np.array([4.0, 4.0, 3.5, 3.0, 2.5, 2.0, 1.0, 0.5])
+    above = np.array([0, 0, 0.5, 0.5, 0.5, 0.5, 1.0, 0.5])
+    rank = np.arange(8) / 7
+    c1 = np.zeros((17, 3), np.float32)
+    cb1 = np.array([-0.75, 0.5, 2.0], np.float32)
+    c2 = np.array([1.5, -2.0, 0.25], np.float32)
+    # unit 0: margin above + 2 phi_7 - 0.75     (active where margin > -0.25)
+    c1[3, 0], c1[5 + 7, 0] = 1.0, 2.0
+    # unit 1: -(v - v1) - 4 phi_8 + 0.5          (active once v1 - v > 1.5)
+    c1[0, 1], c1[5 + 8, 1] = -1.0, -4.0
+    # unit 2: -4 rank + 3 phi_6 + 2              (active while rank < 0.5)
+    c1[2, 2], c1[5 + 6, 2] = -4.0, 3.0
+    w = DgapWeights(np.zeros((12, 2), np.float32), np.zeros(2, np.float32), np.zeros(2, np.float32), 20.0,
+                    c1, cb1, c2, -0.5)
+    h0 = np.maximum(above + 2 * 0.5 - 0.75, 0)
+    h1 = np.maximum(-(v - 4.0) - 4 * 0.5 + 0.5, 0)
+    h2 = np.maximum(-4 * rank + 3 * 0.0 + 2.0, 0)
+    want = 1.5 * h0 - 2.0 * h1 + 0.25 * h2 - 0.5
+    res = dgap.restore(z, 8, w)
+    assert res.corrected
+    assert np.allclose(res.delta, want, rtol=0, atol=1e-12)
+    assert np.allclose(res.logits[[1, 3, 9, 5, 7, 2, 0, 4]], v + want, rtol=0, atol=1e-12)
+    assert res.logits[6] == -1.0 and res.logits[8] == 0.0
