@@ -151,6 +151,22 @@ size_t kvq_workspace_bytes(const kvq_cache* cache);
 kvq_status kvq_decode_attention(const kvq_cache* cache, const void* q, float* out, void* ws,
                                 size_t ws_bytes, void* stream);
 
+/* kvq_decode_attention without a caller workspace, for callers that cannot
+ * allocate device memory (code under graph capture, serving loops that
+ * forbid allocation): the split records live in a scratch array of
+ * KVQ_NOALLOC_SCRATCH_BYTES (16 MiB) that the library holds on every GPU it
+ * runs on until the process ends.  It allocates nothing and launches the
+ * same kernels with the same split plan, so out equals kvq_decode_attention's
+ * bit for bit.  Every call on one GPU uses that GPU's one array: calls that
+ * overlap on one GPU (different streams, or different threads) race and give
+ * undefined outputs; calls ordered on one stream are safe.  The array keeps
+ * the last call's records; nothing in it needs to start at zero.
+ * Errors: KVQ_ERR_ARG (null pointers), KVQ_ERR_CAPACITY when the call would
+ * need more workspace than the array holds (kvq_workspace_bytes at the
+ * current lengths; nothing launched), KVQ_ERR_HIP. */
+#define KVQ_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+kvq_status kvq_decode_attention_noalloc(const kvq_cache* cache, const void* q, float* out, void* stream);
+
 /* One decode step in one call: the same result, cache state and error
  * behaviour as kvq_append(cache, K, V, n_max, n_new, stream) followed by
  * kvq_decode_attention(cache, q, out, ws, ws_bytes, stream) (the decode is

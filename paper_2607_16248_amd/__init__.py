@@ -6,7 +6,7 @@ include/dgap.h, DGAP's logit-side step);
 """
 from .kvq import (KVCache, KvqError, kvq_append, kvq_append_decode, kvq_cache_bytes, kvq_cache_destroy,  # noqa: F401
                   kvq_cache_init, kvq_cache_reset, kvq_check, kvq_chunk_attention, kvq_chunk_workspace_bytes,
-                  kvq_decode_attention,
+                  kvq_decode_attention, kvq_decode_attention_noalloc,
                   kvq_decode_merge, kvq_decode_partials, kvq_dequant,
                   kvq_export, kvq_export_bytes, kvq_free_pages, kvq_last_error, kvq_seq_len, kvq_seq_release,
                   kvq_set_split_tokens,

@@ -31,6 +31,7 @@ SOURCES = [
     ("decode_mfma.hip", ["-fno-honor-nans"]),
     ("dequant.hip", []),
     ("dgap.hip", []),
+    ("noalloc.hip", []),
     ("kvq_api.cpp", []),
 ]
 

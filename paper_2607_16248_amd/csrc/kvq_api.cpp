@@ -22,6 +22,8 @@
 
 using kvq::HeadLayout;
 
+static_assert(kvq::kScratchBytes == KVQ_NOALLOC_SCRATCH_BYTES, "scratch array size as the header states");
+
 struct kvq_cache {
   kvq_cache_desc d{};
   std::vector<uint8_t> bk, bv;
@@ -637,6 +639,24 @@ kvq_status kvq_decode_attention(const kvq_cache* c, const void* q, float* out, v
   if (!q || !out) return fail(KVQ_ERR_ARG, "q and out must be device pointers");
   const SplitPlan p = plan_splits(c);
   kvq_status st = run_partials(c, p, q, ws, ws_bytes, stream);
+  if (st != KVQ_OK) return st;
+  st = run_merge(c, p, ws, out, stream);
+  if (st != KVQ_OK) return st;
+  return ok();
+}
+
+kvq_status kvq_decode_attention_noalloc(const kvq_cache* c, const void* q, float* out, void* stream) {
+  if (!c) return fail(KVQ_ERR_ARG, "cache is NULL");
+  if (!q || !out) return fail(KVQ_ERR_ARG, "q and out must be device pointers");
+  const SplitPlan p = plan_splits(c);
+  const size_t need = (size_t)p.records * c->d.num_q_heads * kvq::kRecFloats * sizeof(float);
+  if (need > kvq::kScratchBytes)
+    return fail(KVQ_ERR_CAPACITY, "this decode needs %zu bytes of workspace, more than the %zu bytes of the "
+                "library's scratch array; use kvq_decode_attention with a caller workspace", need, kvq::kScratchBytes);
+  void* ws = nullptr;
+  const int e = kvq::scratch_workspace(&ws);
+  if (e) return hip_fail(e, "scratch array address");
+  kvq_status st = run_partials(c, p, q, ws, kvq::kScratchBytes, stream);
   if (st != KVQ_OK) return st;
   st = run_merge(c, p, ws, out, stream);
   if (st != KVQ_OK) return st;

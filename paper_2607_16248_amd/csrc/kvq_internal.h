@@ -254,4 +254,10 @@ int launch_dgap(const struct DgapArgs& a, int batch, void* stream);
 int launch_dequant(const DequantArgs& a, void* stream);
 int launch_fill_zero(void* dst, size_t words, void* stream);
 
+// Bytes of the per-device scratch array behind kvq_decode_attention_noalloc.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+// Device address of the current device's scratch array (looked up once per
+// device); returns a hipError_t as int.
+int scratch_workspace(void** ptr);
+
 }  // namespace kvq

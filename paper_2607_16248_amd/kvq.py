@@ -20,7 +20,8 @@ STATUS_NAMES = ["KVQ_OK", "KVQ_ERR_ARG", "KVQ_ERR_UNSUPPORTED", "KVQ_ERR_CAPACIT
 
 EXPORTED = ["kvq_cache_bytes", "kvq_cache_init", "kvq_cache_destroy", "kvq_cache_reset",
             "kvq_seq_len", "kvq_seq_release", "kvq_free_pages",
-            "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention", "kvq_append_decode",
+            "kvq_append", "kvq_workspace_bytes", "kvq_decode_attention", "kvq_decode_attention_noalloc",
+            "kvq_append_decode",
             "kvq_decode_partials", "kvq_decode_merge", "kvq_chunk_workspace_bytes", "kvq_chunk_attention",
             "kvq_dequant", "kvq_export_bytes", "kvq_export", "kvq_check",
             "kvq_set_split_tokens", "kvq_last_error", "kvq_version",
@@ -77,6 +78,7 @@ def lib():
         "kvq_append": ([P, P, P, I32, ctypes.POINTER(I32), P], ctypes.c_int),
         "kvq_workspace_bytes": ([P], S),
         "kvq_decode_attention": ([P, P, P, P, S, P], ctypes.c_int),
+        "kvq_decode_attention_noalloc": ([P, P, P, P], ctypes.c_int),
         "kvq_chunk_workspace_bytes": ([P, ctypes.c_int32], S),
         "kvq_chunk_attention": ([P, P, ctypes.c_int32, P, P, S, P], ctypes.c_int),
         "kvq_append_decode": ([P, P, P, I32, ctypes.POINTER(I32), P, P, P, S, P], ctypes.c_int),
@@ -189,6 +191,11 @@ def kvq_decode_attention(cache: int, q, out, ws, ws_bytes: Optional[int] = None,
     if ws_bytes is None:
         ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().kvq_decode_attention(cache, _ptr(q), _ptr(out), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def kvq_decode_attention_noalloc(cache: int, q, out, stream=None) -> None:
+    """kvq_decode_attention with the library's own scratch array as workspace."""
+    _check(lib().kvq_decode_attention_noalloc(cache, _ptr(q), _ptr(out), _stream(stream)))
 
 
 def kvq_chunk_workspace_bytes(cache: int, n_q: int) -> int:
