@@ -7,7 +7,7 @@
 // over tokens with an online softmax in base 2.  At one or two bits a token
 // of one kv head carries 64-96 bytes but 2 * 4 * 128 multiply-adds, more than
 // the vector ALUs can retire at HBM speed, so both contractions go to the
-// matrix cores with every product exact and fp32 accumulation:
+// matrix cores with fp32 accumulation:
 //
 //   scores:  S[row][t] = sum_c Q'[row][c] * code[t][c] + sum_c q~[row][c] * z[c]
 //     A = Q' = q~ (.) s split into fp16 hi + lo parts (two product terms,
@@ -22,10 +22,15 @@
 //     operand finite; the scale 2^e * log2(e) / sqrt(d) is applied to the
 //     fp32 result.
 //   values:  O^T[c][col] = sum_t code[t][c] * P'[t][col] (+ z term on VALU)
-//     A = value codes (exact fp16), B = P' = p * s_v split hi / lo,
-//     column col = 4*head + value group (one MFMA pair per 4 heads); the
-//     weights p reach the B layout through LDS; output columns whose group
-//     differs from the channel's are discarded.
+//     A = value codes (exact fp16), B = P' = p * s_v rounded once to fp16
+//     (relative error <= 2^-11 per weight, the rounding of the P operand in
+//     any fp16 attention kernel), column col = 4*head + value group (one
+//     MFMA per 4 heads and 16 channels); the weights p reach the B layout
+//     through LDS.  A tile of 16 channels keeps only the columns of its
+//     value group (the rest of its B operand is zero), so tiles of
+//     different groups share one accumulator: two accumulators hold the
+//     128 channels of 4 heads.  (Five heads: the solo quad of head 4 also
+//     carries the residual of P' in its spare columns.)
 //
 // Packed key codes become operands with a shift or two and one AND per
 // element pair: a set bit at mantissa position w of a half is the exact fp16
@@ -285,6 +290,37 @@ struct MatrixStages {
   static constexpr int value = (MatrixOcc<BK, BV, BPG, GQ>::value >= 4 || GQ > 4 || BK + BV >= 16) ? 2 : 3;
 };
 
+// Value-operand halves for every byte of packed value codes, as the words a
+// workgroup copies into LDS: at one bit, byte b gives 8 halves (bit e of b as
+// 0 or 1.0) in 4 words; at two bits, 4 halves (the 2-bit fields of b as 0,
+// 1.0, 2.0, 3.0) in 2 words.  Built at compile time, read from device memory
+// (one 16-byte load per thread) instead of being computed by every
+// workgroup.
+template <int BV>
+struct ValueTable {
+  static constexpr int kWords = BV == 1 ? 256 * 4 : 256 * 2;
+  uint32_t w[kWords];
+};
+constexpr ValueTable<1> make_value_table1() {
+  ValueTable<1> t{};
+  for (int i = 0; i < ValueTable<1>::kWords; ++i) {
+    const int byte = i >> 2, k = i & 3;
+    t.w[i] = (((byte >> (2 * k)) & 1) ? 0x3C00u : 0u) | (((byte >> (2 * k + 1)) & 1) ? 0x3C000000u : 0u);
+  }
+  return t;
+}
+constexpr ValueTable<2> make_value_table2() {
+  ValueTable<2> t{};
+  const uint32_t half_of[4] = {0x0000u, 0x3C00u, 0x4000u, 0x4200u};  // 0, 1, 2, 3 as fp16
+  for (int i = 0; i < ValueTable<2>::kWords; ++i) {
+    const int byte = i >> 1, k = i & 1;
+    t.w[i] = half_of[(byte >> (4 * k)) & 3] | (half_of[(byte >> (4 * k + 2)) & 3] << 16);
+  }
+  return t;
+}
+__device__ const ValueTable<1> kValueTable1 = make_value_table1();
+__device__ const ValueTable<2> kValueTable2 = make_value_table2();
+
 // CAUSAL: chunk queries (rows see tokens below their own limit); the
 // single-token decode instantiations carry no masking code.  PAGED: the
 // packed data live in the pages of a block table (PageMap).
@@ -296,9 +332,15 @@ decode_mfma_kernel(DecodeArgs a) {
   constexpr int NQ = NH / 4;                  // head quads in the value columns
   constexpr int RS = 16 / NH;                 // score rows per head
   constexpr int kDzRows = (kChunk * NH + kQRow - 1) / kQRow;
-  // per wave: Q' hi rows, lo rows, q~ rows, then the zero-point terms of up
-  // to kChunk key groups (16-byte aligned: rows are read with 16-byte loads)
-  __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(3 * NH + kDzRows) * kQRow];
+  // per wave: Q' hi rows, lo rows, then the zero-point terms of up to
+  // kChunk key groups (16-byte aligned: rows are read with 16-byte loads)
+  __shared__ __attribute__((aligned(16))) uint32_t q_lds[kWaves][(2 * NH + kDzRows) * kQRow];
+  // the prepared query, shared by the waves: q~ of head g in row g (the B
+  // operand of the zero-point terms), the lane words of q~ with the key
+  // pair weights, and the fp32 score scale of each head
+  __shared__ __attribute__((aligned(16))) uint32_t qq_s[NH * kQRow];
+  __shared__ uint32_t qt_s[NH][64];
+  __shared__ float cs_s[NH];
   __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * NH];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<GQ> red;
   // value operand halves of each byte of packed codes: 8 halves (bit e of
@@ -319,27 +361,12 @@ decode_mfma_kernel(DecodeArgs a) {
   uint32_t vbound = __builtin_amdgcn_raw_buffer_load_b32(head_rsrc(blk + a.vb, 4), 0, 0, 0);
   asm volatile("" ::: "memory");
 
-  if constexpr (BV == 1) {
-    for (int i = threadIdx.x; i < 256 * 4; i += blockDim.x) {
-      const int byte = i >> 2, k = i & 3;
-      vtab[i] = (((byte >> (2 * k)) & 1) ? 0x3C00u : 0u) | (((byte >> (2 * k + 1)) & 1) ? 0x3C000000u : 0u);
-    }
-    __syncthreads();
-  } else if constexpr (BV == 2) {
-    const uint32_t half_of[4] = {0x0000u, 0x3C00u, 0x4000u, 0x4200u};  // 0, 1, 2, 3 as fp16
-    for (int i = threadIdx.x; i < 256 * 2; i += blockDim.x) {
-      const int byte = i >> 1, k = i & 1;
-      vtab[i] = half_of[(byte >> (4 * k)) & 3] | (half_of[(byte >> (4 * k + 2)) & 3] << 16);
-    }
-    __syncthreads();
-  }
-
   if (wk.sp >= S.nq) {  // fp16 tail tokens: vector path
     float qs0[GQ], qs1[GQ];
     load_q_scaled<GQ, CAUSAL>(a, S, wk.h, wk.rg, lane, qs0, qs1);
     State<GQ> st;
     init_state<GQ>(st);
-    static_assert(kHeadDim * QStride<GQ>::value <= (3 * NH + kDzRows) * kQRow, "tail query fits the Q' area");
+    static_assert(kHeadDim * QStride<GQ>::value <= (2 * NH + kDzRows) * kQRow, "tail query fits the Q' area");
     static_assert(32 * GQ <= kPRow * NH, "tail weights fit the weight area");
     tail_split<GQ, CAUSAL>(a, S, wk.h, wk.rg, blk, qs0, qs1, reinterpret_cast<float*>(q_lds[wv]), p_lds[wv], st,
                            lane, wv);
@@ -430,6 +457,26 @@ decode_mfma_kernel(DecodeArgs a) {
       zq[kb] = __builtin_bit_cast(
           h8_t, ld128(rs, sg + jg * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
   };
+  // The query heads this wave prepares for the workgroup (heads wv,
+  // wv + kWaves, ...), and the value table words this thread copies: both
+  // loads go out before the first blocks', so that the barrier below does
+  // not wait behind the bulk of the data.
+  constexpr int kOwn = (NH + kWaves - 1) / kWaves;
+  uint32_t qw[kOwn];
+#pragma unroll
+  for (int i = 0; i < kOwn; ++i) {
+    const int g = wv + kWaves * i;
+    qw[i] = g < GQ ? reinterpret_cast<const uint32_t*>(qbase + (size_t)(CAUSAL ? a.row_off[g] : g) * kHeadDim)[lane]
+                   : 0u;
+  }
+  constexpr int kTabLoads = BV <= 2 ? ValueTable<BV <= 2 ? BV : 1>::kWords / 4 : 0;
+  u4_t tabw = {0u, 0u, 0u, 0u};
+  if constexpr (kTabLoads > 0) {
+    const uint32_t* tw = BV == 1 ? kValueTable1.w : kValueTable2.w;
+    if ((int)threadIdx.x < kTabLoads) tabw = reinterpret_cast<const u4_t*>(tw)[threadIdx.x];
+  }
+  asm volatile("" ::: "memory");
+
   // the first two blocks and the first zero-points load while the query is prepared
   constexpr int kStages = MatrixStages<BK, BV, BPG, GQ>::value;
   BlockData<BK, BV> b0, b1, b2;
@@ -442,41 +489,47 @@ decode_mfma_kernel(DecodeArgs a) {
 
   // q~ = q * 2^-e per head with max |q~| < 1.  For the code MFMA each lane's
   // channel pair (2*lane, 2*lane+1) also carries 2^-w, w = the bit weight of
-  // those channels in the unpacked key operand.
+  // those channels in the unpacked key operand.  Each wave prepares its own
+  // heads into LDS; empty heads get zero rows (scores 0).
   const float wq = BK == 1 ? ldexpf(1.f, -(lane & 3)) : BK == 2 ? ((lane & 1) ? 0.25f : 1.f) : 1.f;
-  uint32_t* ql = q_lds[wv];
-  uint32_t* qq = ql + 2 * NH * kQRow;  // q~ of head g in row g
-  float* dzt = reinterpret_cast<float*>(ql + 3 * NH * kQRow);  // [group k mod (kChunk / BPG)][head]
-  uint32_t qt[NH];
-  float inv[NH], csc[NH];
 #pragma unroll
-  for (int g = GQ; g < NH; ++g) {  // empty heads: zero rows, scores 0
-    qt[g] = 0u;
-    inv[g] = 0.f;
-    csc[g] = 1.f;
-    qq[g * kQRow + lane] = 0u;
+  for (int i = 0; i < kOwn; ++i) {
+    const int g = wv + kWaves * i;
+    if (g >= NH) break;
+    if (g < GQ) {
+      const float q0 = h2f(qw[i] & 0xFFFF), q1 = h2f(qw[i] >> 16);
+      const float mx = wave_max(fmaxf(fabsf(q0), fabsf(q1)));
+      int e = 0;
+      frexpf(mx, &e);
+      const float inv = ldexpf(1.f, -e);
+      qt_s[g][lane] = h2u((h2_t){(_Float16)(q0 * inv * wq), (_Float16)(q1 * inv * wq)});
+      qq_s[g * kQRow + lane] = h2u((h2_t){(_Float16)(q0 * inv), (_Float16)(q1 * inv)});
+      if (lane == 0) cs_s[g] = ldexpf(a.qscale, e - CodeUnit<BK>::value);  // undoes 2^-e and the code unit
+    } else {
+      qt_s[g][lane] = 0u;
+      qq_s[g * kQRow + lane] = 0u;
+      if (lane == 0) cs_s[g] = 1.f;
+    }
+  }
+  if constexpr (kTabLoads > 0) {
+    if ((int)threadIdx.x < kTabLoads) reinterpret_cast<u4_t*>(vtab)[threadIdx.x] = tabw;
+  }
+  uint32_t* ql = q_lds[wv];
+  float* dzt = reinterpret_cast<float*>(ql + 2 * NH * kQRow);  // [group k mod (kChunk / BPG)][head]
+#pragma unroll
+  for (int g = GQ; g < NH; ++g) {  // empty heads: zero Q' rows
     ql[g * kQRow + lane] = 0u;
     ql[(NH + g) * kQRow + lane] = 0u;
   }
+  __syncthreads();
+  uint32_t qt[NH];
 #pragma unroll
-  for (int g = 0; g < GQ; ++g) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(qbase + (size_t)(CAUSAL ? a.row_off[g] : g) * kHeadDim)[lane];
-    const float q0 = h2f(w & 0xFFFF), q1 = h2f(w >> 16);
-    const float mx = wave_max(fmaxf(fabsf(q0), fabsf(q1)));
-    int e = 0;
-    frexpf(mx, &e);
-    inv[g] = ldexpf(1.f, -e);
-    csc[g] = ldexpf(a.qscale, e - CodeUnit<BK>::value);  // undoes 2^-e and the code unit
-    h2_t t;
-    t.x = (_Float16)(q0 * inv[g] * wq);
-    t.y = (_Float16)(q1 * inv[g] * wq);
-    qt[g] = h2u(t);
-    qq[g * kQRow + lane] = h2u((h2_t){(_Float16)(q0 * inv[g]), (_Float16)(q1 * inv[g])});
-  }
+  for (int g = 0; g < NH; ++g) qt[g] = g < GQ ? qt_s[g][lane] : 0u;
+  const uint32_t* qq = qq_s;
   // score layout: token col of the 16-token tile, heads HPL*row + hh
   float cs[HPL];
 #pragma unroll
-  for (int hh = 0; hh < HPL; ++hh) cs[hh] = pickn<NH>(csc, HPL * row + hh);
+  for (int hh = 0; hh < HPL; ++hh) cs[hh] = cs_s[HPL * row + hh];
   // Chunk queries: row g sees tokens below lim[g]; blocks that reach glim
   // (the row group's smallest limit) mask their later tokens per row.
   // Single-token decode: glim = L, past every packed block.
@@ -537,7 +590,12 @@ decode_mfma_kernel(DecodeArgs a) {
   // Value layout: zacc[q] = the zero-point term of head 4q + hc, group xc
   // over the lane's tokens; acc[q] the code term.
   float m[HPL], l[HPL], zacc[NQ];
-  f4_t acc[NQ][8];
+  // Packed value accumulators: the column group xc of a tile's MFMA keeps
+  // only the columns of its value group, so the four tiles 2j + e (j =
+  // 0..3) with distinct column groups share accumulator e (the other
+  // columns of their B operand are zero).  Tile pair (2j, 2j + 1) takes
+  // column group tile_col(j); lane column xc owns that pair iff they match.
+  f4_t acc[NQ][2];
 #pragma unroll
   for (int hh = 0; hh < HPL; ++hh) {
     m[hh] = -__builtin_inff();
@@ -547,8 +605,15 @@ decode_mfma_kernel(DecodeArgs a) {
   for (int q = 0; q < NQ; ++q) {
     zacc[q] = 0.f;
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb) acc[q][mb] = (f4_t){0.f, 0.f, 0.f, 0.f};
+    for (int e = 0; e < 2; ++e) acc[q][e] = (f4_t){0.f, 0.f, 0.f, 0.f};
   }
+  // Column group of tile pair j: value group g = j * ng / 4 of channels
+  // 32j .. 32j + 31 sits in column groups x with x % ng = g; the pairs
+  // sharing an accumulator take distinct ones.
+  auto tile_col = [&](int j) { return ng == 2 ? (j >> 1) + 2 * (j & 1) : j; };
+  bool own[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) own[j] = xc == tile_col(j);
 
   float* pl = p_lds[wv];
 
@@ -658,7 +723,7 @@ decode_mfma_kernel(DecodeArgs a) {
           av = (H & 1) ? a1 : a0;
         }
 #pragma unroll
-        for (int mb = 0; mb < 8; ++mb) acc[q][mb] *= av;
+        for (int e = 0; e < 2; ++e) acc[q][e] *= av;
         zacc[q] *= av;
       }
     }
@@ -693,9 +758,10 @@ decode_mfma_kernel(DecodeArgs a) {
       const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[Hp * kPRow + 16 + 4 * row]);
       const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
 
-      // P' = p * s_v as fp16 hi + lo: the product and its residual are each
-      // one mixed-precision fma from the fp32 p and the fp16 scale
-      u4_t bhi, blo;
+      // P' = p * s_v rounded once to fp16 (the product is one mixed-precision
+      // fma from the fp32 p and the fp16 scale); the five-head solo quad
+      // also carries the residual in its spare columns
+      u4_t bhi;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const h2_t s2 = u2h(cur.sv[t]);
@@ -709,11 +775,14 @@ decode_mfma_kernel(DecodeArgs a) {
         keep_f32(g0, g1);
         const uint32_t lw = h2u((h2_t){(_Float16)g0, (_Float16)g1});
         bhi[t] = solo ? (hc == 0 ? hw : hc == 1 ? lw : 0u) : hw;
-        blo[t] = lw;
         const h2_t z2 = u2h(cur.zv[t]);
         zacc[q] = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc[q]));
       }
-      const h8_t BH = __builtin_bit_cast(h8_t, bhi), BL = __builtin_bit_cast(h8_t, blo);
+      u4_t bm[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int t = 0; t < 4; ++t) bm[j][t] = own[j] ? bhi[t] : 0u;
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) {
         h8_t av;
@@ -728,8 +797,7 @@ decode_mfma_kernel(DecodeArgs a) {
         } else {
           av = whole8<BV>(&cur.vx[(BV / 4) * mb]);
         }
-        acc[q][mb] = mfma(av, BH, acc[q][mb]);
-        if (!solo) acc[q][mb] = mfma(av, BL, acc[q][mb]);
+        acc[q][mb & 1] = mfma(av, __builtin_bit_cast(h8_t, bm[mb >> 1]), acc[q][mb & 1]);
       }
     }
   };
@@ -795,17 +863,20 @@ decode_mfma_kernel(DecodeArgs a) {
     zs += __shfl_xor(zs, 32);
     const bool solo = GQ == 5 && q == 1;  // head 4: hi columns 0-3, lo columns 4-7
     const int H = solo ? 4 : 4 * q + ehc;
+    // accumulator e of column group exc holds tile 2j + e, tile_col(j) = exc
+    const int ej = ng == 2 ? 2 * (exc & 1) + (exc >> 1) : exc;
 #pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
-      f4_t v = acc[q][mb];
+    for (int e = 0; e < 2; ++e) {
+      f4_t v = acc[q][e];
       if (solo) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] += __shfl_xor(v[e], 4);
+        for (int i = 0; i < 4; ++i) v[i] += __shfl_xor(v[i], 4);
       }
-      if ((solo ? ehc == 0 : H < GQ) && exc == (16 * mb) / a.gv) {
+      if (solo ? ehc == 0 : H < GQ) {
+        const int mb = 2 * ej + e;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + e] = v[e] * kAccScale + zs;
+        for (int i = 0; i < 4; ++i)
+          red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + i] = v[i] * kAccScale + zs;
       }
     }
   }
