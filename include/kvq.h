@@ -269,6 +269,17 @@ kvq_status kvq_check(const kvq_cache* cache, void* stream);
  * changes kvq_workspace_bytes. */
 kvq_status kvq_set_split_tokens(kvq_cache* cache, int32_t tokens);
 
+/* Diagnostics: the device's streaming-read rate, for comparing the decode
+ * kernels' algorithmic bytes with a measured ceiling beside the nominal HBM
+ * peak.  Reads `bytes` (a multiple of 16) from the device buffer `src`
+ * (16-byte aligned) once, with 16-byte loads in a grid-stride loop, and
+ * writes one XOR fold per workgroup to `sink` (device, at least
+ * kvq_read_probe_sink_bytes() bytes, contents meaningless).  Asynchronous on
+ * `stream`; time it with events.  Errors: KVQ_ERR_ARG (null pointer,
+ * misaligned or ragged size), KVQ_ERR_HIP. */
+kvq_status kvq_read_probe(const void* src, size_t bytes, uint32_t* sink, void* stream);
+size_t kvq_read_probe_sink_bytes(void);
+
 /* Message for the last non-OK status on this thread ("" if none). */
 const char* kvq_last_error(void);
 

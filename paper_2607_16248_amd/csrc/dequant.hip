@@ -118,4 +118,39 @@ int launch_dequant(const DequantArgs& a, void* stream) {
   return (int)hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------- read probe
+//
+// Streaming-read ceiling of the device: every thread reads 16-byte words in
+// a grid-stride loop and folds them with XOR; one word per workgroup goes to
+// `sink` so that the loads stay.  The decode kernels' algorithmic bytes are
+// compared with this measured rate as well as with the nominal HBM peak.
+namespace {
+constexpr int kProbeBlocks = 2048;
+__global__ __launch_bounds__(256) void read_probe_kernel(const uint4* __restrict__ src, size_t n, uint32_t* sink) {
+  uint32_t acc = 0u;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    const uint4 v = src[i];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  __shared__ uint32_t red[256];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t x = 0u;
+    for (int t = 0; t < 256; ++t) x ^= red[t];
+    sink[blockIdx.x] = x;
+  }
+}
+}  // namespace
+
+int read_probe_blocks() { return kProbeBlocks; }
+
+int launch_read_probe(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+  if (bytes == 0) return 0;
+  hipLaunchKernelGGL(read_probe_kernel, dim3(kProbeBlocks), dim3(256), 0, (hipStream_t)stream,
+                     static_cast<const uint4*>(src), bytes / 16, sink);
+  return (int)hipGetLastError();
+}
+
 }  // namespace kvq

@@ -958,6 +958,17 @@ kvq_status dgap_restore(const dgap_params* p, float* logits, int32_t batch, void
 
 const char* kvq_last_error(void) { return g_err.c_str(); }
 
+kvq_status kvq_read_probe(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+  if (!src || !sink) return fail(KVQ_ERR_ARG, "src and sink must be device pointers");
+  if (bytes % 16 != 0 || reinterpret_cast<uintptr_t>(src) % 16 != 0)
+    return fail(KVQ_ERR_ARG, "src must be 16-byte aligned and bytes a multiple of 16");
+  const int e = kvq::launch_read_probe(src, bytes, sink, stream);
+  if (e) return hip_fail(e, "read probe launch");
+  return ok();
+}
+
+size_t kvq_read_probe_sink_bytes(void) { return (size_t)kvq::read_probe_blocks() * sizeof(uint32_t); }
+
 const char* kvq_version(void) { return "kvq 0.1.0 gfx950"; }
 
 }  // extern "C"

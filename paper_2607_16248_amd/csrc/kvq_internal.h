@@ -253,6 +253,9 @@ int launch_merge(const MergeArgs& a, void* stream);
 int launch_dgap(const struct DgapArgs& a, int batch, void* stream);
 int launch_dequant(const DequantArgs& a, void* stream);
 int launch_fill_zero(void* dst, size_t words, void* stream);
+// Streaming-read probe: kvq_read_probe's kernel and its grid size.
+int launch_read_probe(const void* src, size_t bytes, uint32_t* sink, void* stream);
+int read_probe_blocks();
 
 // Bytes of the per-device scratch array behind kvq_decode_attention_noalloc.
 constexpr size_t kScratchBytes = (size_t)16 << 20;

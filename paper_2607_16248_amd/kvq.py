@@ -25,6 +25,7 @@ EXPORTED = ["kvq_cache_bytes", "kvq_cache_init", "kvq_cache_destroy", "kvq_cache
             "kvq_decode_partials", "kvq_decode_merge", "kvq_chunk_workspace_bytes", "kvq_chunk_attention",
             "kvq_dequant", "kvq_export_bytes", "kvq_export", "kvq_check",
             "kvq_set_split_tokens", "kvq_last_error", "kvq_version",
+            "kvq_read_probe", "kvq_read_probe_sink_bytes",
             "dgap_workspace_bytes", "dgap_info_floats", "dgap_restore"]
 
 
@@ -91,6 +92,8 @@ def lib():
         "kvq_set_split_tokens": ([P, I32], ctypes.c_int),
         "kvq_last_error": ([], ctypes.c_char_p),
         "kvq_version": ([], ctypes.c_char_p),
+        "kvq_read_probe": ([P, S, P, P], ctypes.c_int),
+        "kvq_read_probe_sink_bytes": ([], S),
         "dgap_workspace_bytes": ([I32, I32, I32], S),
         "dgap_info_floats": ([I32], S),
         "dgap_restore": ([ctypes.POINTER(DgapParams), P, I32, P, S, P, P], ctypes.c_int),
@@ -228,6 +231,15 @@ def kvq_decode_partials(cache: int, q, ws, ws_bytes: Optional[int] = None, strea
     if ws_bytes is None:
         ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().kvq_decode_partials(cache, _ptr(q), _ptr(ws), int(ws_bytes), _stream(stream)))
+
+
+def kvq_read_probe(src, nbytes: int, sink, stream=None) -> None:
+    """Diagnostics: read ``nbytes`` of the device buffer ``src`` once (streaming-read rate)."""
+    _check(lib().kvq_read_probe(_ptr(src), int(nbytes), _ptr(sink), _stream(stream)))
+
+
+def kvq_read_probe_sink_bytes() -> int:
+    return int(lib().kvq_read_probe_sink_bytes())
 
 
 def kvq_decode_merge(cache: int, ws, out, stream=None) -> None:
