@@ -384,42 +384,33 @@ decode_mfma_kernel(DecodeArgs a) {
   // row g of the row group reads q row qbase + row_off[g] (row_off[0] = 0)
   const uint16_t* qbase = CAUSAL ? a.q + q_index<GQ, CAUSAL>(a, S, wk.h, wk.rg, 0) * kHeadDim
                                  : a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * GQ) * kHeadDim;
-  // Packed data: the (sequence, head) region, or in a paged cache the pool,
-  // with every block's page taken from the block table.  The split's first
-  // 64 pages are loaded once, one per lane; a block reads its page's offset
-  // from that lane (pages further on, in splits of more than 64 pages, come
-  // from the table directly).
+  // Packed data: the (sequence, head) region, or in a paged cache this kv
+  // head's region of the page that holds the block (a buffer resource per
+  // block, so that offsets stay inside one page whatever the pool size).
+  // The split's first 64 pages are looked up once, one per lane; a block
+  // reads its page index from that lane (pages further on, in splits of more
+  // than 64 pages, come from the table directly).
   constexpr bool paged = PAGED;
-  const __amdgpu_buffer_rsrc_t rs =
-      paged ? head_rsrc(a.arena + a.pm.pool0, a.pm.pool_bytes) : head_rsrc(blk, a.head_stride);
+  const __amdgpu_buffer_rsrc_t rs = head_rsrc(blk, paged ? 0 : a.head_stride);
   const int32_t* ptab = paged ? a.pm.table + (size_t)S.seq * a.pm.max_pages : nullptr;
-  const uint32_t hoff = paged ? (uint32_t)(wk.h * a.pm.page_head_bytes) : 0u;
+  const uint8_t* pool_h = paged ? a.arena + a.pm.pool0 + (uint64_t)wk.h * a.pm.page_head_bytes : nullptr;
   const int pg0 = paged ? (wk.sp * a.split_tokens) >> a.pm.page_shift : 0;
-  uint32_t lane_pg = 0u;
+  int lane_pg = 0;
   if constexpr (PAGED) {
-    if (pg0 + lane < a.pm.max_pages) lane_pg = (uint32_t)ptab[pg0 + lane] * (uint32_t)a.pm.page_bytes + hoff;
+    if (pg0 + lane < a.pm.max_pages) lane_pg = ptab[pg0 + lane];
   }
-  // offset of the segment holding token tok from the resource base, and
-  // tok's position in it; seg_of takes a wave-uniform token
-  auto seg_of = [&](int tok, int& tin) -> uint32_t {
+  // the resource of the region holding token tok, and tok's position in it;
+  // seg_of takes a wave-uniform token
+  auto seg_of = [&](int tok, int& tin) -> __amdgpu_buffer_rsrc_t {
     if (!paged) {
       tin = tok;
-      return 0u;
+      return rs;
     }
     const int pg = tok >> a.pm.page_shift;
     tin = tok & (a.pm.page_tokens - 1);
     const int k = pg - pg0;
-    return k < 64 ? (uint32_t)__builtin_amdgcn_readlane((int)lane_pg, k)
-                  : (uint32_t)ptab[pg] * (uint32_t)a.pm.page_bytes + hoff;
-  };
-  auto seg_of_lane = [&](int tok, int& tin) -> uint32_t {  // per-lane token
-    if (!paged) {
-      tin = tok;
-      return 0u;
-    }
-    const int pg = tok >> a.pm.page_shift;
-    tin = tok & (a.pm.page_tokens - 1);
-    return (uint32_t)ptab[pg] * (uint32_t)a.pm.page_bytes + hoff;
+    const int pool_pg = k < 64 ? __builtin_amdgcn_readlane(lane_pg, k) : ptab[pg];
+    return head_rsrc(pool_h + (uint64_t)pool_pg * a.pm.page_bytes, a.pm.page_head_bytes);
   };
   LaneOffsets lo;
   lo.km = 4 * lane;
@@ -446,22 +437,30 @@ decode_mfma_kernel(DecodeArgs a) {
   auto load = [&](int i, BlockData<BK, BV>& o) {
     const int j = j0 + kWaves * (i / BPG);
     int tok;
-    const uint32_t sg = seg_of(j * a.gk + (i % BPG) * 32, tok);
+    const __amdgpu_buffer_rsrc_t r = seg_of(j * a.gk + (i % BPG) * 32, tok);
     const int jg = paged ? tok >> a.pm.gk_shift : j;  // key group within the segment
-    load_block<BK, BV>(rs, lo, sg + a.km + (uint32_t)jg * (2 * kHeadDim * 2), sg + a.kc + (uint32_t)tok * 16 * BK,
-                       sg + a.vc + (uint32_t)(tok / 32) * 512 * BV, sg + a.vm + (uint32_t)(tok / 32) * vstride, o);
+    load_block<BK, BV>(r, lo, a.km + (uint32_t)jg * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
+                       a.vc + (uint32_t)(tok / 32) * 512 * BV, a.vm + (uint32_t)(tok / 32) * vstride, o);
   };
   // Key zero-points of the wave's key groups k0 .. k0 + 15 as the A operand
   // of their zero-point terms (row = group; past the last group: the last).
+  // A paged cache reads them with 64-bit addresses (one page per lane).
   auto load_z = [&](int k0, h8_t (&zq)[4]) {
     const int j = j0 + kWaves * min(k0 + col, ngroups - 1);
-    int tin;
-    const uint32_t sg = seg_of_lane(j * a.gk, tin);
-    const uint32_t jg = paged ? (uint32_t)(tin >> a.pm.gk_shift) : (uint32_t)j;
+    if constexpr (PAGED) {
+      const int tok = j * a.gk;
+      const uint8_t* zrow = pool_h + (uint64_t)ptab[tok >> a.pm.page_shift] * a.pm.page_bytes + a.km +
+                            (uint64_t)((tok & (a.pm.page_tokens - 1)) >> a.pm.gk_shift) * (2 * kHeadDim * 2) +
+                            kHeadDim * 2;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-      zq[kb] = __builtin_bit_cast(
-          h8_t, ld128(rs, sg + jg * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
+      for (int kb = 0; kb < 4; ++kb)
+        zq[kb] = __builtin_bit_cast(h8_t, *reinterpret_cast<const u4_t*>(zrow + (32 * kb + 8 * row) * 2));
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        zq[kb] = __builtin_bit_cast(
+            h8_t, ld128(rs, (uint32_t)j * (2 * kHeadDim * 2) + kHeadDim * 2 + (32 * kb + 8 * row) * 2, a.km));
+    }
   };
   // The query heads this wave prepares for the workgroup (heads wv,
   // wv + kWaves, ...), and the value table words this thread copies: both

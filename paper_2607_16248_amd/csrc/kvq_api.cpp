@@ -270,7 +270,7 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   c->cq = packed_capacity(d);
   c->W = d->fp16_window + d->key_group;
   uint64_t off = kvq::kHeaderBytes;
-  uint64_t packed_bytes = 0;  // what the matrix kernel's 32-bit offsets must reach
+  uint64_t packed_bytes = 0;  // what the matrix kernel's 32-bit offsets must reach (one buffer resource)
   if (d->page_tokens > 0) {
     const PagedArena A = paged_arena(d);
     c->paged = true;
@@ -290,7 +290,7 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
     }
     c->pages.assign(d->batch, {});
     for (int pg = A.num_pages - 1; pg >= 0; --pg) c->free_pages.push_back(pg);
-    packed_bytes = c->pm.pool_bytes;
+    packed_bytes = A.page.stride;  // one page's region of one kv head, whatever the pool size
   } else {
     for (int i = 0; i < d->batch; ++i) {
       c->lay.push_back(layout_of(d, c->bk[i], c->bv[i]));

@@ -63,7 +63,7 @@ struct PageMap {
   uint64_t pool0;            // arena offset of pool page 0
   uint64_t page_bytes;       // Hkv * page_head_bytes
   uint64_t page_head_bytes;
-  uint64_t pool_bytes;       // pages * page_bytes (<= 4 GiB for the matrix kernel)
+  uint64_t pool_bytes;       // pages * page_bytes
   int32_t page_tokens, max_pages;
   int32_t page_shift, gk_shift;  // log2(page_tokens), log2(key_group)
 };

@@ -19,7 +19,7 @@ import pytest
 
 import oracle
 from helpers import ATTN_TOL, Case, log, row_rel_err
-from workloads import Workload, gen_q_chunk
+from workloads import Workload, gen_kv, gen_q, gen_q_chunk
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -198,3 +198,53 @@ def test_split_spanning_more_than_64_pages(bk, bv, hq):
         outs.append(o)
     torch.cuda.synchronize()
     assert torch.equal(outs[0], outs[1])
+
+
+def test_pool_larger_than_4_GiB():
+    """A paged pool of 9.7 GB (K8V8, 4096-token pages of 9.4 MB): sequence 0
+    fills 464 pages (4.4 GB), so every page of sequence 1 starts beyond
+    4 GiB of the pool.  The matrix kernel addresses each page through a
+    resource of its own: outputs bit-identical to a contiguous cache (the
+    vector kernel would round differently), and sequence 1 within 2e-3 of
+    the oracle."""
+    from paper_2607_16248_amd import kvq
+    L0, L1, cap, P = 464 * 4096, 6000, 1 << 21, 4096
+    w = W("pool_over_4GiB", 2, 32, 8, (L0, L1), 8, 8, cfg=95)
+    K1, V1 = gen_kv(w, 0, 1)                       # host draw of sequence 1 only
+    q = np.stack([gen_q(w, 0, s) for s in range(2)])
+    caches = [kvq.KVCache(2, 32, 8, cap, [8, 8], [8, 8], key_group=32, value_group=32, device="cuda",
+                          page_tokens=P),
+              kvq.KVCache(2, 32, 8, cap, [8, 8], [8, 8], key_group=32, value_group=32, device="cuda")]
+    assert caches[0].arena.numel() > (9 << 30)
+    g = torch.Generator(device="cuda").manual_seed(4242)
+    step = 131072
+    for t0 in range(0, L0, step):                  # sequence 0: device draws, same rows into both caches
+        n = min(step, L0 - t0)
+        K = torch.randn((1, n, 8, 128), generator=g, device="cuda").half()
+        V = torch.randn((1, n, 8, 128), generator=g, device="cuda").half()
+        Kb = torch.cat([K, torch.zeros_like(K)]), torch.cat([V, torch.zeros_like(V)])
+        for c in caches:
+            c.append(Kb[0], Kb[1], [n, 0])
+        del K, V, Kb
+    Kb = torch.from_numpy(K1[None]).cuda()
+    Vb = torch.from_numpy(V1[None]).cuda()
+    zk = torch.zeros_like(Kb)
+    for c in caches:
+        c.append(torch.cat([zk, Kb]), torch.cat([zk, Vb]), [0, L1])
+    torch.cuda.synchronize()
+    for c in caches:
+        c.check()
+    qd = torch.from_numpy(q).cuda()
+    a = caches[0].decode(qd).cpu().numpy()
+    b = caches[1].decode(qd).cpu().numpy()
+    assert (a.view(np.uint32) == b.view(np.uint32)).all()
+    for h in (0, 7):
+        assert (caches[0].export(1, h) == oracle.build_head(K1[:, h], V1[:, h], 8, 8, 32, 32, 0)).all(), h
+    ref = oracle.decode_seq(q[1], K1, V1, 8, 8, 32, 32, 0)
+    err = row_rel_err(a[1], ref).max()
+    log(f"[paged] pool of {caches[0].arena.numel() / 2**30:.1f} GiB, sequence 1 beyond 4 GiB: "
+        f"max row-relative error {err:.3e}")
+    assert err <= ATTN_TOL
+    del caches
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
