@@ -275,12 +275,11 @@ template <int GQ>
 struct MatrixHeads {
   static constexpr int value = GQ <= 4 ? 4 : 8;
 };
-// Waves per SIMD the instantiation is compiled for: four for 1-bit keys and
-// values with one 32-token block per key group, three for the other 1- and
-// 2-bit four-head cases with one block per group, else two (registers).
+// Waves per SIMD the instantiation is compiled for (matrix_waves, shared
+// with the host's split plan).
 template <int BK, int BV, int BPG, int GQ>
 struct MatrixOcc {
-  static constexpr int value = (GQ > 4 || BK > 2 || BV > 2) ? 2 : BPG == 1 ? (BK + BV == 2 ? 4 : 3) : 2;
+  static constexpr int value = matrix_waves(BK, BV, BPG, GQ);
 };
 // Blocks in flight per wave: at four waves per SIMD, with the eight-head
 // accumulators and with 8-bit blocks (41 registers each), the registers hold
@@ -935,32 +934,7 @@ int launch_bpg(const DecodeArgs& a, int gq, void* stream) {
   }
 }
 
-template <int BK, int BV, int BPG>
-int occ_gq(int gq) {
-  return gq == 4 ? MatrixOcc<BK, BV, BPG, 4>::value : gq == 5 ? MatrixOcc<BK, BV, BPG, 5>::value
-                                                               : MatrixOcc<BK, BV, BPG, 8>::value;
-}
-
-template <int BK, int BV>
-int occ_bpg(int gk, int gq) {
-  return gk == 32 ? occ_gq<BK, BV, 1>(gq) : gk == 64 ? occ_gq<BK, BV, 2>(gq) : occ_gq<BK, BV, 4>(gq);
-}
-
 }  // namespace
-
-int matrix_decode_occupancy(int bk, int bv, int gk, int gq) {
-  if (bk == 1 && bv == 1) return occ_bpg<1, 1>(gk, gq);
-  if (bk == 1 && bv == 2) return occ_bpg<1, 2>(gk, gq);
-  if (bk == 2 && bv == 1) return occ_bpg<2, 1>(gk, gq);
-  if (bk == 2 && bv == 2) return occ_bpg<2, 2>(gk, gq);
-  if (bk == 4) return occ_bpg<4, 4>(gk, gq);
-  return occ_bpg<8, 8>(gk, gq);
-}
-
-bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes) {
-  const bool bits = ((bk == 1 || bk == 2) && (bv == 1 || bv == 2)) || (bk == bv && (bk == 4 || bk == 8));
-  return (gq == 4 || gq == 5 || gq == 8) && bits && gv >= 32 && head_bytes <= 0xFFFFFFFFull;
-}
 
 int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stream) {
   if (a.total_wg <= 0) return 0;

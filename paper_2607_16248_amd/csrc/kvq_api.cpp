@@ -19,6 +19,7 @@
 #include "dgap.h"
 #include "kvq.h"
 #include "kvq_internal.h"
+#include "kvq_layout.h"
 
 using kvq::HeadLayout;
 
@@ -238,6 +239,14 @@ std::vector<std::pair<std::pair<int, int>, std::vector<int>>> bit_classes(const 
 }
 
 }  // namespace
+
+namespace kvq {
+int matrix_decode_occupancy(int bk, int bv, int gk, int gq) { return matrix_waves(bk, bv, gk / 32, gq); }
+
+bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes) {
+  return matrix_heads(gq) && matrix_bits(bk, bv) && gv >= 32 && head_bytes <= 0xFFFFFFFFull;
+}
+}  // namespace kvq
 
 extern "C" {
 
@@ -476,6 +485,9 @@ size_t kvq_workspace_bytes(const kvq_cache* c) {
   return (size_t)c->d.batch * c->d.num_q_heads * (size_t)splits_bound(c) * kvq::kRecFloats * sizeof(float);
 }
 
+}  // extern "C"
+
+// The split plan and the launches of decode, shared by the entry points below.
 namespace {
 
 // Query rows of a launch (see DecodeArgs): nqry queries per sequence in row
@@ -632,6 +644,8 @@ kvq_status run_merge(const kvq_cache* c, const SplitPlan& p, const void* ws, flo
 }
 
 }  // namespace
+
+extern "C" {
 
 kvq_status kvq_decode_attention(const kvq_cache* c, const void* q, float* out, void* ws, size_t ws_bytes,
                                 void* stream) {

@@ -51,6 +51,21 @@
 
 namespace kvq {
 
+// Which caches the matrix-core decode kernel serves: 1- or 2-bit keys and
+// values in any combination, or 4- or 8-bit keys and values of one width;
+// 4, 5 or 8 query heads per kv head; value groups of at least 32 channels.
+KVQ_HD constexpr bool matrix_bits(int bk, int bv) {
+  return ((bk == 1 || bk == 2) && (bv == 1 || bv == 2)) || (bk == bv && (bk == 4 || bk == 8));
+}
+KVQ_HD constexpr bool matrix_heads(int gq) { return gq == 4 || gq == 5 || gq == 8; }
+// Waves per SIMD its instantiations are compiled for: four for 1-bit keys
+// and values with one 32-token block per key group, three for the other 1-
+// and 2-bit four-head cases with one block per group, else two (registers).
+// bpg = key_group / 32.
+KVQ_HD constexpr int matrix_waves(int bk, int bv, int bpg, int gq) {
+  return (gq > 4 || bk > 2 || bv > 2) ? 2 : bpg == 1 ? (bk + bv == 2 ? 4 : 3) : 2;
+}
+
 KVQ_HD inline int pair_bit(int blk4, int e) {
   return 16 * (e & 1) + 8 * (blk4 >> 1) + 4 * (blk4 & 1) + (e >> 1);
 }
