@@ -39,10 +39,13 @@
 // near fp32 precision (see unpack_bits).  An element pair's weight (2^i at
 // one bit, 1 or 4 at two bits) depends only on the channel and is folded
 // into q~ once per decode; the common code unit goes into the fp32 scale.
-// A value operand (8 tokens of one channel) comes from 256-entry LDS tables
-// indexed by bytes of packed codes: one byte at one bit (8 halves, 0 or 1),
-// two bytes at two bits (4 halves each, 0..3), exact normal numbers, one LDS
-// read per byte instead of several vector instructions.
+// A 1-bit value operand (8 tokens of one channel) is unpacked like a key
+// operand (one shift, four ANDs); its element-pair weight 2^i is folded into
+// the softmax weights of those tokens through the exponent offset of their
+// lanes, so it costs no instruction in the loop.  A 2-bit value operand comes
+// from a 256-entry LDS table indexed by bytes of packed codes (4 halves
+// 0..3 per byte, exact normal numbers), one LDS read per byte instead of
+// several vector instructions.
 // At 4 and 8 bits a dword holds whole codes, and one instruction per
 // element pair turns them into subnormal halves (see whole8); a token then
 // carries 160-288 bytes for the same arithmetic, and the matrix cores keep
@@ -289,36 +292,25 @@ struct MatrixStages {
   static constexpr int value = (MatrixOcc<BK, BV, BPG, GQ>::value >= 4 || GQ > 4 || BK + BV >= 16) ? 2 : 3;
 };
 
-// Value-operand halves for every byte of packed value codes, as the words a
-// workgroup copies into LDS: at one bit, byte b gives 8 halves (bit e of b as
-// 0 or 1.0) in 4 words; at two bits, 4 halves (the 2-bit fields of b as 0,
-// 1.0, 2.0, 3.0) in 2 words.  Built at compile time, read from device memory
-// (one 16-byte load per thread) instead of being computed by every
-// workgroup.
-template <int BV>
-struct ValueTable {
-  static constexpr int kWords = BV == 1 ? 256 * 4 : 256 * 2;
+// Value-operand halves for every byte of packed 2-bit value codes, as the
+// words a workgroup copies into LDS: byte b gives 4 halves (the 2-bit fields
+// of b as 0, 1.0, 2.0, 3.0) in 2 words.  Built at compile time, read from
+// device memory (one 16-byte load per thread) instead of being computed by
+// every workgroup.
+struct ValueTable2 {
+  static constexpr int kWords = 256 * 2;
   uint32_t w[kWords];
 };
-constexpr ValueTable<1> make_value_table1() {
-  ValueTable<1> t{};
-  for (int i = 0; i < ValueTable<1>::kWords; ++i) {
-    const int byte = i >> 2, k = i & 3;
-    t.w[i] = (((byte >> (2 * k)) & 1) ? 0x3C00u : 0u) | (((byte >> (2 * k + 1)) & 1) ? 0x3C000000u : 0u);
-  }
-  return t;
-}
-constexpr ValueTable<2> make_value_table2() {
-  ValueTable<2> t{};
+constexpr ValueTable2 make_value_table2() {
+  ValueTable2 t{};
   const uint32_t half_of[4] = {0x0000u, 0x3C00u, 0x4000u, 0x4200u};  // 0, 1, 2, 3 as fp16
-  for (int i = 0; i < ValueTable<2>::kWords; ++i) {
+  for (int i = 0; i < ValueTable2::kWords; ++i) {
     const int byte = i >> 1, k = i & 1;
     t.w[i] = half_of[(byte >> (4 * k)) & 3] | (half_of[(byte >> (4 * k + 2)) & 3] << 16);
   }
   return t;
 }
-__device__ const ValueTable<1> kValueTable1 = make_value_table1();
-__device__ const ValueTable<2> kValueTable2 = make_value_table2();
+__device__ const ValueTable2 kValueTable2 = make_value_table2();
 
 // CAUSAL: chunk queries (rows see tokens below their own limit); the
 // single-token decode instantiations carry no masking code.  PAGED: the
@@ -342,9 +334,8 @@ decode_mfma_kernel(DecodeArgs a) {
   __shared__ float cs_s[NH];
   __shared__ __attribute__((aligned(16))) float p_lds[kWaves][kPRow * NH];  // weights to the value layout; fp16 tail split
   __shared__ Reduce<GQ> red;
-  // value operand halves of each byte of packed codes: 8 halves (bit e of
-  // the byte) at 1 bit, 4 halves (the 2-bit fields) at 2 bits
-  constexpr int kTabWords = BV == 1 ? 256 * 4 : BV == 2 ? 256 * 2 : 4;
+  // value operand halves of each byte of packed 2-bit codes (its 2-bit fields)
+  constexpr int kTabWords = BV == 2 ? ValueTable2::kWords : 4;
   __shared__ __attribute__((aligned(16))) uint32_t vtab[kTabWords];
 
   const Work wk = find_work<CAUSAL>(a);
@@ -473,11 +464,10 @@ decode_mfma_kernel(DecodeArgs a) {
     qw[i] = g < GQ ? reinterpret_cast<const uint32_t*>(qbase + (size_t)(CAUSAL ? a.row_off[g] : g) * kHeadDim)[lane]
                    : 0u;
   }
-  constexpr int kTabLoads = BV <= 2 ? ValueTable<BV <= 2 ? BV : 1>::kWords / 4 : 0;
+  constexpr int kTabLoads = BV == 2 ? ValueTable2::kWords / 4 : 0;
   u4_t tabw = {0u, 0u, 0u, 0u};
   if constexpr (kTabLoads > 0) {
-    const uint32_t* tw = BV == 1 ? kValueTable1.w : kValueTable2.w;
-    if ((int)threadIdx.x < kTabLoads) tabw = reinterpret_cast<const u4_t*>(tw)[threadIdx.x];
+    if ((int)threadIdx.x < kTabLoads) tabw = reinterpret_cast<const u4_t*>(kValueTable2.w)[threadIdx.x];
   }
   asm volatile("" ::: "memory");
 
@@ -591,9 +581,20 @@ decode_mfma_kernel(DecodeArgs a) {
 
   // Score layout: m[hh] = the softmax reference of head HPL*row + hh
   // (uniform over the row), l[hh] = the sum of the lane's own weights.
-  // Value layout: zacc[q] = the zero-point term of head 4q + hc, group xc
-  // over the lane's tokens; acc[q] the code term.
-  float m[HPL], l[HPL], zacc[NQ];
+  // Value layout: zacc[q][t] = the zero-point term of head 4q + hc, group xc
+  // over the lane's tokens (element pair t of the 1-bit value operand: the
+  // weights of pair t carry 2^-t there); acc[q] the code term.
+  //
+  // 1-bit values: the unpacked operand of element pair i is code * 2^(i - 18),
+  // so the weights of its tokens are taken as 2^-i * p.  Score lane col holds
+  // block token 16*mb + col, which is element 4*mb + (col & 3) of the value
+  // operand, pair i = 2*mb + pw with pw = (col & 3) >> 1: the exponent offset
+  // nm[hh][mb] = -(m + i) gives the weighted p at no extra cost, and l adds
+  // 4x the second tile's weight and is rescaled by 2^pw after the loop.
+  constexpr bool kPairW = BV == 1;
+  constexpr int NZ = kPairW ? 4 : 1;
+  const float pw = kPairW ? (float)((col & 3) >> 1) : 0.f;
+  float m[HPL], l[HPL], nm[HPL][2], zacc[NQ][NZ];
   // Packed value accumulators: the column group xc of a tile's MFMA keeps
   // only the columns of its value group, so the four tiles 2j + e (j =
   // 0..3) with distinct column groups share accumulator e (the other
@@ -604,10 +605,12 @@ decode_mfma_kernel(DecodeArgs a) {
   for (int hh = 0; hh < HPL; ++hh) {
     m[hh] = -__builtin_inff();
     l[hh] = 0.f;
+    nm[hh][0] = nm[hh][1] = __builtin_inff();
   }
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
-    zacc[q] = 0.f;
+#pragma unroll
+    for (int t = 0; t < NZ; ++t) zacc[q][t] = 0.f;
 #pragma unroll
     for (int e = 0; e < 2; ++e) acc[q][e] = (f4_t){0.f, 0.f, 0.f, 0.f};
   }
@@ -713,6 +716,8 @@ decode_mfma_kernel(DecodeArgs a) {
         alpha[hh] = CAUSAL && mnew == m[hh] ? 1.f : __builtin_amdgcn_exp2f(m[hh] - mnew);
         l[hh] *= alpha[hh];
         m[hh] = mnew;
+        nm[hh][0] = -(mnew + pw);
+        nm[hh][1] = kPairW ? nm[hh][0] - 2.f : nm[hh][0];
       }
       // the same factors in the value layout: head H = 4q + hc sits in the
       // score lanes of row H / HPL, as their element H % HPL
@@ -728,7 +733,8 @@ decode_mfma_kernel(DecodeArgs a) {
         }
 #pragma unroll
         for (int e = 0; e < 2; ++e) acc[q][e] *= av;
-        zacc[q] *= av;
+#pragma unroll
+        for (int t = 0; t < NZ; ++t) zacc[q][t] *= av;
       }
     }
     // to the value layout: lane (col, row) needs tokens 4*row + 0..3 and
@@ -736,13 +742,13 @@ decode_mfma_kernel(DecodeArgs a) {
     float e[HPL][2];
 #pragma unroll
     for (int hh = 0; hh < HPL; ++hh) {
-      e[hh][0] = __builtin_amdgcn_exp2f(fmaf(raw[hh][0], cs[hh], -m[hh]));
-      e[hh][1] = __builtin_amdgcn_exp2f(fmaf(raw[hh][1], cs[hh], -m[hh]));
+      e[hh][0] = __builtin_amdgcn_exp2f(fmaf(raw[hh][0], cs[hh], nm[hh][0]));
+      e[hh][1] = __builtin_amdgcn_exp2f(fmaf(raw[hh][1], cs[hh], nm[hh][1]));
       if (masked) {  // masked tokens weigh 0, also while m is still -inf
         e[hh][0] = raw[hh][0] == -__builtin_inff() ? 0.f : e[hh][0];
         e[hh][1] = raw[hh][1] == -__builtin_inff() ? 0.f : e[hh][1];
       }
-      l[hh] += e[hh][0] + e[hh][1];
+      l[hh] += kPairW ? fmaf(e[hh][1], 4.f, e[hh][0]) : e[hh][0] + e[hh][1];
     }
     wave_lds_sync();
 #pragma unroll
@@ -780,7 +786,8 @@ decode_mfma_kernel(DecodeArgs a) {
         const uint32_t lw = h2u((h2_t){(_Float16)g0, (_Float16)g1});
         bhi[t] = solo ? (hc == 0 ? hw : hc == 1 ? lw : 0u) : hw;
         const h2_t z2 = u2h(cur.zv[t]);
-        zacc[q] = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, zacc[q]));
+        float& za = zacc[q][kPairW ? t : 0];
+        za = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, za));
       }
       u4_t bm[4];
 #pragma unroll
@@ -791,8 +798,7 @@ decode_mfma_kernel(DecodeArgs a) {
       for (int mb = 0; mb < 8; ++mb) {
         h8_t av;
         if constexpr (BV == 1) {
-          const uint32_t byte = (cur.vx[mb >> 2] >> (8 * (mb & 3))) & 0xFFu;
-          av = *reinterpret_cast<const h8_t*>(&vtab[byte * 4]);
+          av = unpack_bits(cur.vx[mb >> 2], mb & 3);
         } else if constexpr (BV == 2) {
           const uint32_t x = cur.vx[mb >> 1] >> (16 * (mb & 1));
           const uint2 t0 = *reinterpret_cast<const uint2*>(&vtab[(x & 0xFFu) * 2]);
@@ -849,20 +855,24 @@ decode_mfma_kernel(DecodeArgs a) {
   // the loop's register budget free of epilogue-only values.
   const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int ecol = ln & 15, erow = ln >> 4, ehc = ecol >> 2, exc = ecol & 3;
-  // l: sum the 16 lanes of the head's row; zacc: sum over the lane rows
-  // (the tokens of a group column)
+  // l: sum the 16 lanes of the head's row (1-bit values: the lane's weights
+  // carry 2^-pw); zacc: sum over the lane rows (the tokens of a group column)
 #pragma unroll
   for (int hh = 0; hh < HPL; ++hh) {
+    if constexpr (kPairW) l[hh] *= (ecol & 2) ? 2.f : 1.f;
     l[hh] += dpp_mov<kQuadXor1>(0.f, l[hh]);
     l[hh] += dpp_mov<kQuadXor2>(0.f, l[hh]);
     l[hh] += dpp_mov<kHalfMirror>(0.f, l[hh]);
     l[hh] += dpp_mov<kMirror>(0.f, l[hh]);
   }
-  // whole value codes enter the products as code * 2^CodeUnit
-  const float kAccScale = BV <= 2 ? 1.f : ldexpf(1.f, -CodeUnit<BV>::value);
+  // 1-bit, 4- and 8-bit value codes enter the products as code * 2^CodeUnit
+  // (2-bit table halves are the codes themselves)
+  const float kAccScale = BV == 2 ? 1.f : ldexpf(1.f, -CodeUnit<BV>::value);
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
-    float zs = zacc[q];
+    float zs = zacc[q][0];
+#pragma unroll
+    for (int t = 1; t < NZ; ++t) zs = fmaf(zacc[q][t], (float)(1 << t), zs);
     zs += __shfl_xor(zs, 16);
     zs += __shfl_xor(zs, 32);
     const bool solo = GQ == 5 && q == 1;  // head 4: hi columns 0-3, lo columns 4-7

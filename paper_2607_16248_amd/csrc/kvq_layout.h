@@ -27,8 +27,9 @@
 //      dwords; operand mb (channels 16*mb .. 16*mb + 15, channel c =
 //      16*mb + c%16) has elements e' (0..7) for block tokens r = tau(8*kg + e'),
 //      tau(8*kg + e') = 4*kg + e' for e' < 4 and 16 + 4*kg + (e' - 4) otherwise.
-//      b = 1: dword mb >> 2, bit 8*(mb&3) + e': one byte per operand, looked
-//             up in a 256-entry table of 8 halves;
+//      b = 1: dword mb >> 2, bit pair_bit(mb&3, e'): like 1-bit keys, element
+//             pair i at bits (s, s + 16), s = 4*(mb&3) + i, so one shift and
+//             four ANDs per operand make its halves;
 //      b = 2: dword mb >> 1, bits 16*(mb&1) + 2*e': two bytes per operand,
 //             each looked up in a 256-entry table of 4 halves;
 //      b = 4: dword mb, nibble (e'>>1) + 4*(e'&1);
@@ -122,7 +123,7 @@ KVQ_HD inline BitLoc value_bit(int r, int c, int p, int b) {
   const int kg = r16 >> 2, e = (r16 & 3) + 4 * hi;
   const int mb = c >> 4;
   const int lane = (c & 15) + 16 * kg;
-  if (b == 1) return {lane * 2 + (mb >> 2), 8 * (mb & 3) + e};
+  if (b == 1) return {lane * 2 + (mb >> 2), pair_bit(mb & 3, e)};
   if (b == 2) return {lane * 4 + (mb >> 1), 16 * (mb & 1) + 2 * e + p};
   return {lane * 2 * b + (b / 4) * mb + elem_word(e, b), b * elem_field(e, b) + p};
 }
@@ -132,8 +133,8 @@ KVQ_HD inline void value_bit_owner(int w, int q, int b, int& r, int& c, int& p) 
   const int lane = w / (2 * b), o = w % (2 * b);
   int mb, e;
   if (b == 1) {
-    mb = 4 * o + (q >> 3);
-    e = q & 7;
+    mb = 4 * o + 2 * ((q >> 3) & 1) + ((q >> 2) & 1);
+    e = 2 * (q & 3) + (q >> 4);
     p = 0;
   } else if (b == 2) {
     mb = 2 * o + (q >> 4);

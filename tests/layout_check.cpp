@@ -6,7 +6,7 @@
 // 2. Packing random codes with the inverse maps and unpacking one MFMA
 //    operand the way the decode kernel does (shifts, ANDs, byte permutes,
 //    byte tables) gives back each element's code times the operand's fixed
-//    weight.
+//    weight (per element pair at one bit).
 // Prints "ok" and exits 0, or prints the first mismatch and exits 1.
 #include <cmath>
 #include <cstdint>
@@ -109,9 +109,9 @@ static void key_operand(const uint32_t* row, int b, int g, int kb, uint32_t w[4]
 static void value_operand(const uint32_t* blk, int b, int L, int mb, uint32_t w[4]) {
   const uint32_t* x = blk + 2 * b * L;
   if (b == 1) {
-    const uint32_t byte = (x[mb >> 2] >> (8 * (mb & 3))) & 0xFF;
-    for (int k = 0; k < 4; ++k)
-      w[k] = (((byte >> (2 * k)) & 1) ? 0x3C00u : 0u) | (((byte >> (2 * k + 1)) & 1) ? 0x3C000000u : 0u);
+    const int sh = 4 * (mb & 3) - 6;
+    const uint32_t src = sh > 0 ? x[mb >> 2] >> sh : x[mb >> 2] << -sh;
+    for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (6 + i));
   } else if (b == 2) {
     const uint32_t half_of[4] = {0x0000u, 0x3C00u, 0x4000u, 0x4200u};
     const uint32_t v = x[mb >> 1] >> (16 * (mb & 1));
@@ -173,7 +173,9 @@ static int check_operands(int b, std::mt19937& rng) {
       kvq::value_bit_owner(w, q, b, r, c, p);
       blk[w] |= (uint32_t)((vc[r * 128 + c] >> p) & 1) << q;
     }
-  const double vunit = b <= 2 ? 1.0 : std::ldexp(1.0, b == 4 ? -20 : -24);
+  // 1-bit operands carry the key-style pair weight 2^i and unit 2^-18 (the
+  // kernel folds 2^-i into the weights p); 2-bit table halves are exact codes
+  const double vunit = b == 2 ? 1.0 : std::ldexp(1.0, b == 1 ? -18 : b == 4 ? -20 : -24);
   for (int L = 0; L < 64; ++L)
     for (int mb = 0; mb < 8; ++mb) {
       uint32_t w[4];
@@ -181,7 +183,9 @@ static int check_operands(int b, std::mt19937& rng) {
       for (int e = 0; e < 8; ++e) {
         const uint32_t h = (w[e >> 1] >> (16 * (e & 1))) & 0xFFFF;
         const int r = kvq::value_token(L >> 4, e), c = 16 * mb + (L & 15);
-        if (half_value(h) != vc[r * 128 + c] * vunit) return fail("value operand", b, L, mb, e);
+        const double vweight = b == 1 ? std::ldexp(1.0, e >> 1) : 1.0;
+        if (half_value(h) != vc[r * 128 + c] * vweight * vunit) return fail("value operand", b, L, mb, e);
+        if (b == 1 && (h >> 10)) return fail("value operand not subnormal", b, L, mb, e);
       }
     }
   return 0;
