@@ -29,6 +29,7 @@ SOURCES = [
     ("append.hip", ["-ffp-contract=off"]),
     ("decode.hip", ["-fno-honor-nans"]),
     ("decode_mfma.hip", ["-fno-honor-nans"]),
+    ("chunk_mfma.hip", ["-fno-honor-nans"]),
     ("dequant.hip", []),
     ("dgap.hip", []),
     ("noalloc.hip", []),

@@ -60,9 +60,10 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// floats per channel of the query rows staged for the vector passes
 template <int GQ>
 struct QStride {
-  static constexpr int value = GQ <= 4 ? GQ : 8;
+  static constexpr int value = GQ <= 4 ? GQ : GQ <= 8 ? 8 : 16;
 };
 
 template <int GQ>
@@ -206,10 +207,13 @@ __device__ __forceinline__ int group_limit(const DecodeArgs& a, const DecodeSeq&
   return S.L - a.nqry + 1 + rg * a.qpr;
 }
 
+// (g0: the first row of the group the GQ rows start at; the 16-row chunk
+// kernel takes its fp16 tail in two halves of 8 rows)
 template <int GQ>
-__device__ __forceinline__ void row_limits(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int (&lim)[GQ]) {
+__device__ __forceinline__ void row_limits(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int (&lim)[GQ],
+                                           int g0 = 0) {
 #pragma unroll
-  for (int g = 0; g < GQ; ++g) lim[g] = row_limit(a, S, rg, g);
+  for (int g = 0; g < GQ; ++g) lim[g] = row_limit(a, S, rg, g0 + g);
 }
 
 // Per-wave partial results of GQ query heads, staged for the combine.
@@ -248,7 +252,7 @@ __device__ __forceinline__ void stage_state(State<GQ>& st, Reduce<GQ>& r, int la
 // split sp for the GQ query heads of kv head h.
 template <int GQ, bool CHUNK>
 __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int sp,
-                                             const Reduce<GQ>& r) {
+                                             const Reduce<GQ>& r, int g0 = 0) {
   for (int idx = threadIdx.x; idx < GQ * kHeadDim; idx += blockDim.x) {
     const int g = idx / kHeadDim, c = idx % kHeadDim;
     float M = -__builtin_inff();
@@ -265,7 +269,7 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSe
       lsum = fmaf(f, r.l[w][g], lsum);
     }
     const size_t rows = CHUNK ? (size_t)a.hq * a.nqry : (size_t)a.hq;
-    float* rec = a.ws + ((size_t)(S.ws_base + sp) * rows + rec_row<GQ, CHUNK>(a, h, rg, g)) * kRecFloats;
+    float* rec = a.ws + ((size_t)(S.ws_base + sp) * rows + rec_row<GQ, CHUNK>(a, h, rg, g0 + g)) * kRecFloats;
     rec[4 + c] = val;
     if (c == 0) { rec[0] = M; rec[1] = lsum; }
   }
@@ -275,7 +279,7 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSe
 template <int GQ, bool CHUNK>
 __device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq& S, int h, int rg,
                                            const uint8_t* blk, const float (&qs0)[GQ], const float (&qs1)[GQ],
-                                           float* qp, float* pl, State<GQ>& st, int lane, int wv) {
+                                           float* qp, float* pl, State<GQ>& st, int lane, int wv, int g0 = 0) {
   constexpr int QS = QStride<GQ>::value;
   // Fused append: this workgroup alone reads the ring of (sequence, head h)
   // in this launch; it first stores the tokens appended by the call, which
@@ -302,7 +306,7 @@ __device__ __forceinline__ void tail_split(const DecodeArgs& a, const DecodeSeq&
   }
   wave_lds_sync();
   int lim[GQ];
-  row_limits<GQ>(a, S, h, rg, lim);
+  row_limits<GQ>(a, S, h, rg, lim, g0);
   for (int pass = wv; pass * 32 < S.L - S.Lq; pass += kWaves)
     tail_pass<GQ, CHUNK>(a, S, blk, pass, qp, pl, st, lim, lane);
 }
@@ -322,10 +326,10 @@ __device__ __forceinline__ void init_state(State<GQ>& st) {
 // pre-scaled to base 2.
 template <int GQ, bool CHUNK>
 __device__ __forceinline__ void load_q_scaled(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int lane,
-                                              float (&qs0)[GQ], float (&qs1)[GQ]) {
+                                              float (&qs0)[GQ], float (&qs1)[GQ], int g0 = 0) {
 #pragma unroll
   for (int g = 0; g < GQ; ++g) {
-    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + q_index<GQ, CHUNK>(a, S, h, rg, g) * kHeadDim)[lane];
+    const uint32_t w = reinterpret_cast<const uint32_t*>(a.q + q_index<GQ, CHUNK>(a, S, h, rg, g0 + g) * kHeadDim)[lane];
     qs0[g] = h2f(w & 0xFFFF) * a.qscale;
     qs1[g] = h2f(w >> 16) * a.qscale;
   }

@@ -56,16 +56,14 @@
 #include "decode_common.h"
 #include "kvq_internal.h"
 #include "kvq_layout.h"
+#include "mfma_common.h"
 
 namespace kvq {
 namespace {
 
 using namespace dec;
 
-typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
-typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
-typedef float f4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
+using namespace mfma_ops;
 
 // Headroom of the softmax reference above the largest score seen (log2
 // units): weights of later tokens within it need no rescale.
@@ -80,94 +78,6 @@ constexpr int kPRow = 48;
 // the table holds the zero-point terms of the kChunk / BPG key groups a wave
 // processes next.
 constexpr int kChunk = 48;
-
-__device__ __forceinline__ h2_t u2h(uint32_t v) { return __builtin_bit_cast(h2_t, v); }
-__device__ __forceinline__ uint32_t h2u(h2_t v) { return __builtin_bit_cast(uint32_t, v); }
-
-// One MFMA operand (8 halves) from the 1-bit codes of 4-element block blk4
-// in x: element pair i sits at bits (s, s + 16), s = pair_bit(blk4, 2i) =
-// 4*blk4 + i.  One shift moves the block to mantissa positions 6 + i, and one
-// AND per pair leaves each half equal to bit * 2^(6 + i - 24), an exact fp16
-// subnormal whose set bit is among the top mantissa bits 6..9.  (The matrix
-// cores add the products of subnormal fp16 inputs to about 2^-(13 + p)
-// relative precision for a set bit at mantissa position p; at 6..9 that is
-// 2^-19 or better.)  The other operand carries 2^-i.
-__device__ __forceinline__ h8_t unpack_bits(uint32_t x, int blk4) {
-  const int sh = 4 * blk4 - 6;
-  const uint32_t src = sh > 0 ? x >> sh : x << -sh;
-  u4_t w;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) w[i] = src & (0x10001u << (6 + i));
-  return __builtin_bit_cast(h8_t, w);
-}
-
-// One MFMA operand from 2-bit codes: operand k (0, 1) of dword x holds
-// element pair i at bits 8k + 2i and 8k + 2i + 16.  Two shifts put pairs 0
-// and 1 (then 2 and 3) at mantissa bits 6-7 and 8-9, and one AND per pair
-// keeps them: halves code * 2^(6 - 24) for pairs 0, 2 and code * 2^(8 - 24)
-// for pairs 1, 3 (the other operand carries 1/4 for those).
-__device__ __forceinline__ h8_t unpack_pairs2(uint32_t x, int k) {
-  const uint32_t y1 = k ? x >> 2 : x << 6, y2 = k ? x >> 6 : x << 2;
-  u4_t w;
-  w[0] = y1 & 0x00C000C0u;
-  w[1] = y1 & 0x03000300u;
-  w[2] = y2 & 0x00C000C0u;
-  w[3] = y2 & 0x03000300u;
-  return __builtin_bit_cast(h8_t, w);
-}
-
-// One MFMA operand from whole 4- or 8-bit codes (elements e = 0..7 of the
-// operand, layout in kvq_layout.h): each half is code * 2^(U - 24), an exact
-// fp16 subnormal with the code at mantissa bits U .. U + B - 1 (U = 0 for
-// 8 bits, 4 for 4 bits), one instruction per element pair (a byte permute,
-// or a shift and an AND).
-template <int B>
-__device__ __forceinline__ h8_t whole8(const uint32_t* x) {
-  u4_t w;
-  if constexpr (B == 8) {
-    // dword h holds elements 4h .. 4h + 3 in its bytes; the selector puts
-    // bytes (2i, 2i + 1) into the low bytes of the two halves (0x0C = zero)
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      w[2 * h] = __builtin_amdgcn_perm(0u, x[h], 0x0C010C00u);
-      w[2 * h + 1] = __builtin_amdgcn_perm(0u, x[h], 0x0C030C02u);
-    }
-  } else {
-    // element pair i at nibbles (i, i + 4): moved to bits (4, 20)
-    w[0] = (x[0] << 4) & 0x00F000F0u;
-    w[1] = x[0] & 0x00F000F0u;
-    w[2] = (x[0] >> 4) & 0x00F000F0u;
-    w[3] = (x[0] >> 8) & 0x00F000F0u;
-  }
-  return __builtin_bit_cast(h8_t, w);
-}
-
-// Weights p reach up to 2^S instead of 1 so that p * s_v, a B operand in
-// fp16 hi + lo halves, stays clear of the fp16 subnormal range, where it
-// would lose its low bits (small value scales: few-bit codes of values with
-// a small range, or 4- and 8-bit codes, whose scale is range / 15 or / 255).
-// S is chosen per (sequence, kv head) from the bound the append kernel keeps
-// on the head's value scales: 2^S * bound < 2^15 (p <= 1 before the shift).
-// Every split record carries its own reference, so the merge needs no
-// common S.
-constexpr int kMaxPShift = 30;
-
-// log2 of one code unit in a key operand (the lowest element pair sits at
-// mantissa bit 6 at 1 and 2 bits, whole codes at bits 4.. and 0..), and in a
-// value operand (1 and 2 bits come from tables of exact normal halves).
-template <int B>
-struct CodeUnit {
-  static constexpr int value = B <= 2 ? 6 - 24 : B == 4 ? 4 - 24 : -24;
-};
-
-// Keeps two fp32 results as such: an fma whose result is only converted to
-// fp16 would otherwise become v_fma_mixlo/mixhi_f16, which issue at half the
-// rate of v_fma_mix_f32 plus one v_cvt_pk_f16_f32 per pair.
-__device__ __forceinline__ void keep_f32(float& a, float& b) { asm("" : "+v"(a), "+v"(b)); }
-
-__device__ __forceinline__ f4_t mfma(h8_t a, h8_t b, f4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
 
 // Maximum over the four lane rows (lanes l, l^16, l^32, l^48) with the
 // gfx950 row-swap permutes.
@@ -192,27 +102,6 @@ __device__ __forceinline__ float pick_from(const float (&v)[N], int i) {
 template <int N>
 __device__ __forceinline__ float pickn(const float (&v)[N], int i) {
   return pick_from<0, N>(v, i);
-}
-
-// Buffer resource over one (sequence, kv head) block.  Every load is
-// base + per-lane offset + uniform offset: the per-block part is scalar
-// arithmetic and the vector ALU does no address math.  The host keeps the
-// block under 4 GiB for this kernel.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t head_rsrc(const uint8_t* base, uint64_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, (int)(uint32_t)bytes,
-                                           0x00020000);
-}
-
-__device__ __forceinline__ uint32_t ld32(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t s) {
-  return __builtin_amdgcn_raw_buffer_load_b32(r, v, s, 0);
-}
-__device__ __forceinline__ uint2 ld64(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t s) {
-  typedef uint32_t u2 __attribute__((ext_vector_type(2)));
-  const u2 x = __builtin_amdgcn_raw_buffer_load_b64(r, v, s, 0);
-  return make_uint2(x[0], x[1]);
-}
-__device__ __forceinline__ u4_t ld128(__amdgpu_buffer_rsrc_t r, uint32_t v, uint32_t s) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, v, s, 0);
 }
 
 // Everything one 32-token block reads from memory.
@@ -292,25 +181,6 @@ struct MatrixStages {
   static constexpr int value = (MatrixOcc<BK, BV, BPG, GQ>::value >= 4 || GQ > 4 || BK + BV >= 16) ? 2 : 3;
 };
 
-// Value-operand halves for every byte of packed 2-bit value codes, as the
-// words a workgroup copies into LDS: byte b gives 4 halves (the 2-bit fields
-// of b as 0, 1.0, 2.0, 3.0) in 2 words.  Built at compile time, read from
-// device memory (one 16-byte load per thread) instead of being computed by
-// every workgroup.
-struct ValueTable2 {
-  static constexpr int kWords = 256 * 2;
-  uint32_t w[kWords];
-};
-constexpr ValueTable2 make_value_table2() {
-  ValueTable2 t{};
-  const uint32_t half_of[4] = {0x0000u, 0x3C00u, 0x4000u, 0x4200u};  // 0, 1, 2, 3 as fp16
-  for (int i = 0; i < ValueTable2::kWords; ++i) {
-    const int byte = i >> 1, k = i & 1;
-    t.w[i] = half_of[(byte >> (4 * k)) & 3] | (half_of[(byte >> (4 * k + 2)) & 3] << 16);
-  }
-  return t;
-}
-__device__ const ValueTable2 kValueTable2 = make_value_table2();
 
 // CAUSAL: chunk queries (rows see tokens below their own limit); the
 // single-token decode instantiations carry no masking code.  PAGED: the

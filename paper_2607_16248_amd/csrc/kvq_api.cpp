@@ -497,19 +497,23 @@ struct Rows {
 };
 
 // Single-token decode: one row group of the kv head's query heads.  Chunk
-// queries: the largest row group a kernel has (matrix: 4, 5, 8 rows; vector:
-// also 1, 2) made of whole queries, with a whole number of groups.
-Rows rows_for(const kvq_cache* c, bool matrix, int nqry) {
+// queries: the largest row group a kernel has (matrix: 16 rows in the chunk
+// kernel for 1-, 2- and 4-bit classes with value groups of 32 channels, 4,
+// 5, 8 in the decode kernel; vector: also 1, 2) made of whole queries, with
+// a whole number of groups.
+Rows rows_for(const kvq_cache* c, bool matrix, int nqry, int bk, int bv) {
   const int gqh = c->d.num_q_heads / c->d.num_kv_heads;
   Rows r;
   r.rows = gqh;
   if (nqry <= 1) return r;
-  static const int kMatrixRows[] = {8, 5, 4}, kVectorRows[] = {8, 5, 4, 2, 1};
+  static const int kMatrixRows[] = {16, 8, 5, 4}, kVectorRows[] = {8, 5, 4, 2, 1};
   const int* cand = matrix ? kMatrixRows : kVectorRows;
-  const int ncand = matrix ? 3 : 5;
+  const int ncand = matrix ? 4 : 5;
+  const bool rows16 = matrix && c->d.value_group == 32 && bk + bv <= 8;
   r.nqry = nqry;
   for (int k = 0; k < ncand; ++k) {
     const int rg = cand[k];
+    if (rg == 16 && !rows16) continue;
     if (rg % gqh == 0 && nqry % (rg / gqh) == 0) {
       r.qpr = rg / gqh;
       r.nrg = nqry / r.qpr;
@@ -537,7 +541,7 @@ SplitPlan plan_splits(const kvq_cache* c, int nqry = 1) {
   for (int i = 0; i < B; ++i) classes[{c->bk[i], c->bv[i]}].push_back(i);
   for (auto& cl : classes) {
     const bool matrix = c->matrix[cl.second[0]] != 0;
-    const Rows r = rows_for(c, matrix, nqry);
+    const Rows r = rows_for(c, matrix, nqry, cl.first.first, cl.first.second);
     const int occ = nqry > 1 && matrix
                         ? kvq::matrix_decode_occupancy(cl.first.first, cl.first.second, c->d.key_group, r.rows)
                         : 0;
@@ -590,9 +594,9 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.hq = d.num_q_heads; a.hkv = d.num_kv_heads; a.gk = d.key_group; a.gv = d.value_group; a.W = c->W;
     a.split_tokens = p.st[cls.second[0]];
     a.qscale = qscale;
-    const Rows r = rows_for(c, c->matrix[cls.second[0]] != 0, p.nqry);
+    const Rows r = rows_for(c, c->matrix[cls.second[0]] != 0, p.nqry, cls.first.first, cls.first.second);
     a.nqry = r.nqry; a.qpr = r.qpr; a.nrg = r.nrg; a.gqh = d.num_q_heads / d.num_kv_heads;
-    for (int g = 0; g < 8; ++g) {
+    for (int g = 0; g < 16; ++g) {
       a.row_x[g] = g / a.gqh;
       a.row_off[g] = a.row_x[g] * d.num_q_heads + g % a.gqh;
     }
@@ -614,9 +618,9 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     }
     a.nseq = n;
     a.total_wg = wg;
-    const int e = c->matrix[cls.second[0]]
-                      ? kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, r.rows, stream)
-                      : kvq::launch_decode(a, cls.first.first, cls.first.second, r.rows, stream);
+    const int e = !c->matrix[cls.second[0]] ? kvq::launch_decode(a, cls.first.first, cls.first.second, r.rows, stream)
+                  : r.rows == 16       ? kvq::launch_chunk_matrix(a, cls.first.first, cls.first.second, stream)
+                                       : kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, r.rows, stream);
     if (e) return hip_fail(e, "decode launch");
   }
   return KVQ_OK;

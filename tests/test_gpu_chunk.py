@@ -75,6 +75,10 @@ CASES = [
     (W("k1v4_gq4_vector", 1, 32, 8, 800, 1, 4), 9),                  # vector kernel, 4-row groups
     (W("ragged_mixed_g64", 3, 32, 8, (900, 64, 300), (1, 2, 4), (1, 2, 4), gk=64), 33),
     (W("whole_sequence", 1, 32, 8, 48, 1, 1), 48),                   # n_q = L
+    # 16-row groups (the chunk kernel): 2 queries x 8 heads, and 4 x 4 over
+    # two ragged sequences with 64-token key groups and 1-bit values
+    (W("k4v4_gq8_rows16", 1, 64, 8, 900, 4, 4), 6),
+    (W("k2v1_gq4_rows16_g64", 2, 32, 8, (1000, 517), 2, 1, gk=64), 8),
 ]
 
 
