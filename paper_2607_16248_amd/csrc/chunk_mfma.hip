@@ -42,27 +42,27 @@ using namespace dec;
 using namespace mfma_ops;
 
 constexpr int kRows = 16;           // rows of a row group
-constexpr float kMargin = 3.f;      // lazy softmax reference headroom (log2 units)
+constexpr float kMargin = 6.f;      // lazy softmax reference headroom (log2 units)
 constexpr int kQR = 68;             // dwords per Q' row (64 + 4: rows start in distinct bank quads)
 constexpr int kPR = 36;             // floats per weight row (32 + 4)
 constexpr int kZG = 16;             // key groups per zero-point table
 
-// LDS areas (bytes).  The Q' rows of the waves are overlaid by the staged
-// query words before the loop and by the cross-wave reduction after it.
+// LDS areas (bytes).  The first holds the cross-wave reduction after the
+// loop, or the staged query rows of the fp16-tail splits (per wave).
+constexpr int kTailQ = kHeadDim * 8;  // floats of one wave's staged query rows (8 rows)
 constexpr int kOffQA = 0;
-constexpr int kBytesQA = kWaves * 2 * kRows * kQR * 4;
-constexpr int kOffPL = kOffQA + kBytesQA;
+constexpr int kBytesQA = (int)sizeof(Reduce<8>);  // the reduction takes 8 rows at a time
+constexpr int kOffPL = (kOffQA + kBytesQA + 15) / 16 * 16;
 constexpr int kOffVM = kOffPL + kWaves * kRows * kPR * 4;
-constexpr int kOffDZ = kOffVM + kWaves * 128 * 4;
+constexpr int kOffKS = kOffVM + kWaves * 128 * 4;
+constexpr int kOffDZ = kOffKS + kWaves * 64 * 4;
 constexpr int kOffQQ = kOffDZ + kWaves * kZG * kRows * 4;
 constexpr int kOffCS = kOffQQ + kRows * kQR * 4;
 constexpr int kOffVT = kOffCS + kRows * 4;
 constexpr int kSmemBytes = kOffVT + ValueTable2::kWords * 4;
-static_assert(sizeof(Reduce<kRows>) <= kBytesQA, "the reduction fits the Q' area");
-static_assert(kRows * 64 * 4 <= kBytesQA, "the query words fit the Q' area");
-static_assert(kHeadDim * 8 * 4 <= 2 * kRows * kQR * 4, "a tail half's query fits its wave's Q' area");
+static_assert(kWaves * kTailQ * 4 <= kBytesQA, "the tail splits' query rows fit the first area");
 static_assert(32 * 8 <= kRows * kPR, "a tail half's weights fit its wave's weight area");
-static_assert(sizeof(Reduce<8>) <= kBytesQA, "a tail half's reduction fits the Q' area");
+static_assert(sizeof(Reduce<8>) <= kBytesQA, "8 rows of the reduction fit the first area");
 
 // Everything one 32-token block reads from memory.
 template <int BK, int BV>
@@ -73,8 +73,14 @@ struct ChunkBlock {
   uint2 vm;            // bytes 8*lane .. 8*lane + 7 of the block's value meta (staged in LDS)
 };
 
+template <int BK, int BV>
+struct ChunkOcc {  // waves per SIMD (registers), shared with the host's split plan
+  static constexpr int value = chunk_waves(BK, BV);
+};
+
 template <int BK, int BV, int BPG, bool PAGED>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void chunk_mfma_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ChunkOcc<BK, BV>::value))) void
+chunk_mfma_kernel(DecodeArgs a) {
   constexpr int R = kRows;
   constexpr bool kPairW = BV == 1;  // 1-bit value operands carry pair weights 2^t
   __shared__ __attribute__((aligned(16))) uint8_t smem[kSmemBytes];
@@ -85,8 +91,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   uint32_t* const qq_s = reinterpret_cast<uint32_t*>(smem + kOffQQ);
   float* const cs_s = reinterpret_cast<float*>(smem + kOffCS);
   uint32_t* const vtab = reinterpret_cast<uint32_t*>(smem + kOffVT);
-  uint32_t* const qt_s = qa_all;  // [R][64], before the loop
-  Reduce<R>& red = *reinterpret_cast<Reduce<R>*>(smem + kOffQA);
+  uint32_t* const ks_all = reinterpret_cast<uint32_t*>(smem + kOffKS);
+  Reduce<8>& red = *reinterpret_cast<Reduce<8>*>(smem + kOffQA);
 
   const Work wk = find_work<true>(a);
   const DecodeSeq& S = a.seq[wk.si];
@@ -96,8 +102,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   asm volatile("" ::: "memory");
 
   if (wk.sp >= S.nq) {  // fp16 tail tokens: the vector path, in two halves of 8 rows
-    Reduce<8>& red8 = *reinterpret_cast<Reduce<8>*>(smem + kOffQA);
-    uint32_t* qa = qa_all + wv * 2 * R * kQR;
+    uint32_t* qa = qa_all + wv * kTailQ;
     for (int half = 0; half < 2; ++half) {
       float qs0[8], qs1[8];
       load_q_scaled<8, true>(a, S, wk.h, wk.rg, lane, qs0, qs1, 8 * half);
@@ -106,9 +111,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
       tail_split<8, true>(a, S, wk.h, wk.rg, blk, qs0, qs1, reinterpret_cast<float*>(qa), pl_all + wv * R * kPR, st,
                           lane, wv, 8 * half);
       __syncthreads();  // every wave is done with its area before the reduction overlays it
-      stage_state<8>(st, red8, lane, wv);
+      stage_state<8>(st, red, lane, wv);
       __syncthreads();
-      write_record<8, true>(a, S, wk.h, wk.rg, wk.sp, red8, 8 * half);
+      write_record<8, true>(a, S, wk.h, wk.rg, wk.sp, red, 8 * half);
       __syncthreads();  // the reduction is read before the next half's query overlays it
     }
     return;
@@ -228,9 +233,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     load_z(0, zq);
   }
 
-  // q~ = q * 2^-e per row with max |q~| < 1; the key pair weights of the
-  // lane's channels (2^-w) ride on the Q' words
-  const float wq = BK == 1 ? ldexpf(1.f, -(lane & 3)) : BK == 2 ? ((lane & 1) ? 0.25f : 1.f) : 1.f;
+  // q~ = q * 2^-e per row with max |q~| < 1
 #pragma unroll
   for (int i = 0; i < R / kWaves; ++i) {
     const int g = wv + kWaves * i;
@@ -239,7 +242,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     int e = 0;
     frexpf(mx, &e);
     const float inv = ldexpf(1.f, -e);
-    qt_s[g * 64 + lane] = h2u((h2_t){(_Float16)(q0 * inv * wq), (_Float16)(q1 * inv * wq)});
     qq_s[g * kQR + lane] = h2u((h2_t){(_Float16)(q0 * inv), (_Float16)(q1 * inv)});
     if (lane == 0) cs_s[g] = ldexpf(a.qscale, e - CodeUnit<BK>::value);
   }
@@ -247,9 +249,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     if ((int)threadIdx.x < kTabLoads) reinterpret_cast<u4_t*>(vtab)[threadIdx.x] = tabw;
   }
   __syncthreads();
-  uint32_t qt[R];
+  // q~ of row col in the A layout of the score product (channels 32*kb +
+  // 8*row + e), with the key operand's pair weights: element pair t of a
+  // 1-bit operand carries 2^t, odd pairs of a 2-bit operand 4
+  h8_t qa[4];
 #pragma unroll
-  for (int g = 0; g < R; ++g) qt[g] = qt_s[g * 64 + lane];
+  for (int kb = 0; kb < 4; ++kb) {
+    const u4_t v = *reinterpret_cast<const u4_t*>(&qq_s[col * kQR + 16 * kb + 4 * row]);
+    u4_t w;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const _Float16 f = (_Float16)(BK == 1 ? ldexpf(1.f, -t) : (BK == 2 && (t & 1)) ? 0.25f : 1.f);
+      w[t] = h2u(u2h(v[t]) * (h2_t){f, f});
+    }
+    qa[kb] = __builtin_bit_cast(h8_t, w);
+  }
   float cs[4];
   int lim[4];
 #pragma unroll
@@ -258,9 +272,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     lim[r] = row_limit(a, S, wk.rg, 4 * row + r);
   }
   const int glim = group_limit(a, S, wk.rg);
-  __syncthreads();  // the query words (in the Q' area) are read
 
-  uint32_t* const qa = qa_all + wv * 2 * R * kQR;
+  uint32_t* const ks = ks_all + wv * 64;
   float* const pl = pl_all + wv * R * kPR;
   uint32_t* const vml = vm_all + wv * 128;
   float* const dzt = dz_all + wv * kZG * R;
@@ -327,7 +340,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 #pragma unroll
   for (int t = 0; t < 8; ++t) acc[t] = (f4_t){0.f, 0.f, 0.f, 0.f};
 
-  h8_t ahi[4], alo[4];
   f4_t dz = {0.f, 0.f, 0.f, 0.f};
   auto process = [&](const ChunkBlock<BK, BV>& cur, int i) {
     if (BPG == 1 || i % BPG == 0) {
@@ -336,38 +348,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         fill_dz(zq);
         if (k + kZG < ngroups) load_z(k + kZG, zq);
       }
-      // Q' = q~ (.) s of the block's key group, hi and lo rows, to the A layout
+      // the key scales of the block's key group go through LDS (lane L
+      // holds channels 2L, 2L+1)
       wave_lds_sync();
-#pragma unroll
-      for (int g = 0; g < R; ++g) {
-        const h2_t q2 = u2h(qt[g]), s2 = u2h(cur.s);
-        const h2_t hi = q2 * s2;
-        const h2_t lo = __builtin_elementwise_fma(q2, s2, -hi);
-        qa[g * kQR + lane] = h2u(hi);
-        qa[(R + g) * kQR + lane] = h2u(lo);
-      }
+      ks[lane] = cur.s;
       wave_lds_sync();
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        ahi[kb] = *reinterpret_cast<const h8_t*>(&qa[col * kQR + 16 * kb + 4 * row]);
-        alo[kb] = *reinterpret_cast<const h8_t*>(&qa[(R + col) * kQR + 16 * kb + 4 * row]);
-      }
       dz = *reinterpret_cast<const f4_t*>(&dzt[(k % kZG) * R + 4 * row]);
     }
 
-    // scores of token 16*mb + col, rows 4*row + r
-    f4_t d[2];
+    // scores of token 16*mb + col, rows 4*row + r; Q' = q~ (.) s of each
+    // 32-channel block kb in the A layout, hi and lo parts
+    f4_t d[2] = {dz, dz};
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      d[mb] = dz;
+    for (int kb = 0; kb < 4; ++kb) {
+      const u4_t sv = *reinterpret_cast<const u4_t*>(&ks[16 * kb + 4 * row]);
+      const u4_t qv = __builtin_bit_cast(u4_t, qa[kb]);
+      u4_t h, o;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
+      for (int t = 0; t < 4; ++t) {
+        const h2_t hi = u2h(qv[t]) * u2h(sv[t]);
+        h[t] = h2u(hi);
+        o[t] = h2u(__builtin_elementwise_fma(u2h(qv[t]), u2h(sv[t]), -hi));
+      }
+      const h8_t ahi = __builtin_bit_cast(h8_t, h), alo = __builtin_bit_cast(h8_t, o);
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
         h8_t b;
         if constexpr (BK == 1) b = unpack_bits(cur.kx[mb][0], kb);
         else if constexpr (BK == 2) b = unpack_pairs2(cur.kx[mb][kb >> 1], kb & 1);
         else b = whole8<BK>(&cur.kx[mb][(BK / 4) * kb]);
-        d[mb] = mfma(ahi[kb], b, d[mb]);
-        d[mb] = mfma(alo[kb], b, d[mb]);
+        d[mb] = mfma(ahi, b, d[mb]);
+        d[mb] = mfma(alo, b, d[mb]);
       }
     }
     const int tok = (j0 + kWaves * (i / BPG)) * a.gk + (i % BPG) * 32;
@@ -385,36 +396,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
           if (tok + 16 * mb + col >= lim[r]) raw[r][mb] = -__builtin_inff();
     }
 
-    // online softmax (base 2) per row, lazy reference as in the decode kernel
+    // online softmax (base 2) per row, lazy reference as in the decode
+    // kernel; lane row r of the 4 row blocks rescales only when one of
+    // those rows moves its reference
     const float ninf = -__builtin_inff();
-    float bm[4];
-    bool up = false;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      bm[r] = fmaf(fmaxf(raw[r][0], raw[r][1]), cs[r], -pshift);
-      up |= bm[r] > m[r];
-    }
-    if (__builtin_amdgcn_ballot_w64(up)) {
-      float alpha[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float b = bm[r];
+      const float bmr = fmaf(fmaxf(raw[r][0], raw[r][1]), cs[r], -pshift);
+      if (__builtin_amdgcn_ballot_w64(bmr > m[r])) {
+        float b = bmr;
         b = fmaxf(b, dpp_mov<kQuadXor1>(ninf, b));
         b = fmaxf(b, dpp_mov<kQuadXor2>(ninf, b));
         b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
         b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
         const float mnew = b > m[r] ? b + kMargin : m[r];
         // a row with no visible token yet keeps m = -inf and factor 1
-        alpha[r] = mnew == m[r] ? 1.f : __builtin_amdgcn_exp2f(m[r] - mnew);
-        l[r] *= alpha[r];
+        const float alpha = mnew == m[r] ? 1.f : __builtin_amdgcn_exp2f(m[r] - mnew);
+        l[r] *= alpha;
         m[r] = mnew;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc[t][r] *= alpha;
+        zac[r] *= alpha;
       }
-#pragma unroll
-      for (int t = 0; t < 8; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) acc[t][r] *= alpha[r];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) zac[r] *= alpha[r];
     }
     float e[4][2];
 #pragma unroll
@@ -518,25 +521,33 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     l[r] += dpp_mov<kMirror>(0.f, l[r]);
   }
   const float kAccScale = ldexpf(1.f, (BV == 2 ? 0 : -CodeUnit<BV>::value) - xshift);
-  __syncthreads();  // every wave is done with its Q' area before the reduction overlays it
+  float zg[4][4];  // zero-point terms of rows 4*erow + r, group g, in this lane
 #pragma unroll
-  for (int mb = 0; mb < 8; ++mb) {
-    const int g = mb / 2;
+  for (int g = 0; g < 4; ++g)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float z = __shfl(zac[r], 16 * erow + g);
-      red.acc[wv][(4 * erow + r) * kHeadDim + 16 * mb + ecol] = acc[mb][r] * kAccScale + z;
+    for (int r = 0; r < 4; ++r) zg[g][r] = __shfl(zac[r], 16 * erow + g);
+  // rows 8*half .. 8*half + 7 (lane row blocks 2*half, 2*half + 1) pass
+  // through the reduction area one half after the other
+  for (int half = 0; half < 2; ++half) {
+    __syncthreads();  // the area is free
+    if ((erow >> 1) == half) {
+      const int rb = erow & 1;
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          red.acc[wv][(4 * rb + r) * kHeadDim + 16 * mb + ecol] = acc[mb][r] * kAccScale + zg[mb / 2][r];
+      if (ecol == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          red.m[wv][4 * rb + r] = m[r];
+          red.l[wv][4 * rb + r] = l[r];
+        }
+      }
     }
+    __syncthreads();
+    write_record<8, true>(a, S, wk.h, wk.rg, wk.sp, red, 8 * half);
   }
-  if (ecol == 0) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      red.m[wv][4 * erow + r] = m[r];
-      red.l[wv][4 * erow + r] = l[r];
-    }
-  }
-  __syncthreads();
-  write_record<R, true>(a, S, wk.h, wk.rg, wk.sp, red);
 }
 
 template <int BK, int BV, int BPG>
