@@ -1,6 +1,6 @@
 // Matrix-core decode attention for caches with 1- or 2-bit keys and values,
-// or 4- or 8-bit keys and values of one width, and 4, 5 or 8 query heads per
-// kv head (gfx950, v_mfma_f32_16x16x32_f16).
+// or 4- or 8-bit keys and values, and 4, 5 or 8 query heads per kv head
+// (gfx950, v_mfma_f32_16x16x32_f16).
 //
 // Same result as the vector kernel: softmax(q K^T / sqrt(d)) V over the
 // dequantized cache (Introduction: scaled dot-product attention), split-K
@@ -823,6 +823,8 @@ int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stre
   if (bk == 2 && bv == 1) return launch_bpg<2, 1>(a, gq, stream);
   if (bk == 2 && bv == 2) return launch_bpg<2, 2>(a, gq, stream);
   if (bk == 4 && bv == 4) return launch_bpg<4, 4>(a, gq, stream);
+  if (bk == 4 && bv == 8) return launch_bpg<4, 8>(a, gq, stream);
+  if (bk == 8 && bv == 4) return launch_bpg<8, 4>(a, gq, stream);
   if (bk == 8 && bv == 8) return launch_bpg<8, 8>(a, gq, stream);
   return (int)hipErrorInvalidValue;
 }

@@ -51,6 +51,10 @@ SMALL = [
     W("gq5_k8v8_R128_t3", 2, 40, 8, (1200, 300), 8, 8, R=128, dist="student_t3"),
     W("gq8_k4v4_g128", 1, 64, 8, 1500, 4, 4, gk=128),
     W("k8v8_g64_gv64_L2000", 1, 32, 8, 2000, 8, 8, gk=64, gv=64),
+    # 4- and 8-bit keys and values of different widths on the matrix cores
+    W("k4v8_gq4_L1300", 1, 32, 8, 1300, 4, 8),
+    W("k8v4_gq5_g64_R40", 2, 40, 8, (900, 1100), 8, 4, gk=64, R=40),
+    W("gq8_k4v8_gv64", 1, 64, 8, 700, 4, 8, gv=64),
 ]
 
 
