@@ -65,8 +65,8 @@ def matrix_path(w) -> bool:
 
 def source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("csrc/decode.hip", "csrc/decode_mfma.hip", "csrc/decode_common.h", "csrc/kvq_internal.h",
-              "csrc/kvq_layout.h", "build.py"):
+    for f in ("csrc/decode.hip", "csrc/decode_mfma.hip", "csrc/chunk_mfma.hip", "csrc/mfma_common.h",
+              "csrc/decode_common.h", "csrc/kvq_internal.h", "csrc/kvq_layout.h", "build.py"):
         with open(os.path.join(ROOT, "paper_2607_16248_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
