@@ -25,20 +25,25 @@ COMMON = [f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 
+# The matrix-core decode source is compiled once per bit class (its kernels
+# are many template instantiations), so that the classes build in parallel.
+MATRIX_CLASSES = [(1, 1), (1, 2), (2, 1), (2, 2), (4, 4), (4, 8), (8, 4), (8, 8)]
+
 SOURCES = [
-    ("append.hip", ["-ffp-contract=off"]),
-    ("decode.hip", ["-fno-honor-nans"]),
-    ("decode_mfma.hip", ["-fno-honor-nans"]),
-    ("chunk_mfma.hip", ["-fno-honor-nans"]),
-    ("dequant.hip", []),
-    ("dgap.hip", []),
-    ("noalloc.hip", []),
-    ("kvq_api.cpp", []),
-]
+    ("append.hip", ["-ffp-contract=off"], None),
+    ("decode.hip", ["-fno-honor-nans"], None),
+    ("chunk_mfma.hip", ["-fno-honor-nans"], None),
+    ("dequant.hip", [], None),
+    ("dgap.hip", [], None),
+    ("noalloc.hip", [], None),
+    ("matrix_dispatch.cpp", [], None),
+    ("kvq_api.cpp", [], None),
+] + [("decode_mfma.hip", ["-fno-honor-nans", f"-DKVQ_BK={bk}", f"-DKVQ_BV={bv}"], f"decode_mfma_k{bk}v{bv}.o")
+     for bk, bv in MATRIX_CLASSES]
 
 
-def _compile(src, extra, verbose):
-    obj = os.path.join(BUILD, src + ".o")
+def _compile(src, extra, verbose, obj_name=None):
+    obj = os.path.join(BUILD, obj_name or src + ".o")
     cmd = [HIPCC] + COMMON + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -53,8 +58,13 @@ def _compile(src, extra, verbose):
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s[0], s[1], verbose), SOURCES))
+    workers = min(len(SOURCES), max(2, os.cpu_count() or 2))
+    # the long compiles first, so that they start at once
+    order = sorted(range(len(SOURCES)), key=lambda i: SOURCES[i][0] not in ("decode_mfma.hip", "chunk_mfma.hip"))
+    with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+        done = dict(zip(order, ex.map(lambda i: _compile(SOURCES[i][0], SOURCES[i][1], verbose, SOURCES[i][2]),
+                                      order)))
+    objs = [done[i] for i in range(len(SOURCES))]
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:

@@ -1,5 +1,5 @@
 // Matrix-core decode attention for caches with 1- or 2-bit keys and values,
-// or 4- or 8-bit keys and values, and 4, 5 or 8 query heads per kv head
+// or 4- or 8-bit keys and values, and 1, 2, 4, 5 or 8 query heads per kv head
 // (gfx950, v_mfma_f32_16x16x32_f16).
 //
 // Same result as the vector kernel: softmax(q K^T / sqrt(d)) V over the
@@ -797,6 +797,12 @@ int launch_t(const DecodeArgs& a, void* stream) {
 template <int BK, int BV, int BPG>
 int launch_gq(const DecodeArgs& a, int gq, void* stream) {
   switch (gq) {
+    case 1:  // one or two query heads per kv head: 32-token key groups only
+      if constexpr (BPG == 1) return launch_t<BK, BV, BPG, 1>(a, stream);
+      return (int)hipErrorInvalidValue;
+    case 2:
+      if constexpr (BPG == 1) return launch_t<BK, BV, BPG, 2>(a, stream);
+      return (int)hipErrorInvalidValue;
     case 4: return launch_t<BK, BV, BPG, 4>(a, stream);
     case 5: return launch_t<BK, BV, BPG, 5>(a, stream);
     case 8: return launch_t<BK, BV, BPG, 8>(a, stream);
@@ -816,17 +822,12 @@ int launch_bpg(const DecodeArgs& a, int gq, void* stream) {
 
 }  // namespace
 
-int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stream) {
-  if (a.total_wg <= 0) return 0;
-  if (bk == 1 && bv == 1) return launch_bpg<1, 1>(a, gq, stream);
-  if (bk == 1 && bv == 2) return launch_bpg<1, 2>(a, gq, stream);
-  if (bk == 2 && bv == 1) return launch_bpg<2, 1>(a, gq, stream);
-  if (bk == 2 && bv == 2) return launch_bpg<2, 2>(a, gq, stream);
-  if (bk == 4 && bv == 4) return launch_bpg<4, 4>(a, gq, stream);
-  if (bk == 4 && bv == 8) return launch_bpg<4, 8>(a, gq, stream);
-  if (bk == 8 && bv == 4) return launch_bpg<8, 4>(a, gq, stream);
-  if (bk == 8 && bv == 8) return launch_bpg<8, 8>(a, gq, stream);
-  return (int)hipErrorInvalidValue;
+// This source is compiled once per bit class (KVQ_BK key bits, KVQ_BV value
+// bits, set by the build), so that the classes' kernels build in parallel;
+// each object holds one class's launcher (launch_decode_matrix dispatches).
+template <>
+int launch_matrix_class<KVQ_BK, KVQ_BV>(const DecodeArgs& a, int gq, void* stream) {
+  return launch_bpg<KVQ_BK, KVQ_BV>(a, gq, stream);
 }
 
 }  // namespace kvq

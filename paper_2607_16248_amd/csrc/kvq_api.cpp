@@ -243,8 +243,8 @@ std::vector<std::pair<std::pair<int, int>, std::vector<int>>> bit_classes(const 
 namespace kvq {
 int matrix_decode_occupancy(int bk, int bv, int gk, int gq) { return matrix_waves(bk, bv, gk / 32, gq); }
 
-bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes) {
-  return matrix_heads(gq) && matrix_bits(bk, bv) && gv >= 32 && head_bytes <= 0xFFFFFFFFull;
+bool matrix_decode_supported(int bk, int bv, int gq, int gk, int gv, uint64_t head_bytes) {
+  return matrix_heads(gq, gk) && matrix_bits(bk, bv) && gv >= 32 && head_bytes <= 0xFFFFFFFFull;
 }
 }  // namespace kvq
 
@@ -311,6 +311,7 @@ kvq_status kvq_cache_init(kvq_cache** out, const kvq_cache_desc* d, void* arena,
   c->Lq.assign(d->batch, 0);
   for (int i = 0; i < d->batch; ++i)
     c->matrix.push_back(kvq::matrix_decode_supported(c->bk[i], c->bv[i], d->num_q_heads / d->num_kv_heads,
+                                                     d->key_group,
                                                      d->value_group, c->paged ? packed_bytes : c->lay[i].stride)
                             ? 1
                             : 0);

@@ -244,12 +244,16 @@ int launch_decode_matrix(const DecodeArgs& a, int bk, int bv, int gq, void* stre
 // Matrix-core decode (and the matrix layout) for this bit class: 4, 5 or 8
 // query heads per kv head, 1- or 2-bit codes, value groups >= 32 channels,
 // and a (sequence, head) block that one buffer resource covers.
-bool matrix_decode_supported(int bk, int bv, int gq, int gv, uint64_t head_bytes);
+bool matrix_decode_supported(int bk, int bv, int gq, int gk, int gv, uint64_t head_bytes);
 // Waves per SIMD of the matrix-core kernel for this bit class (2, 3 or 4);
 // the vector kernel runs two.
 int matrix_decode_occupancy(int bk, int bv, int gk, int gq);
 // Chunk queries over 16-row groups (chunk_mfma.hip).
 int launch_chunk_matrix(const DecodeArgs& a, int bk, int bv, void* stream);
+// The matrix-core decode kernels of one bit class (decode_mfma.hip, one
+// object per class); launch_decode_matrix (matrix_dispatch.cpp) picks one.
+template <int BK, int BV>
+int launch_matrix_class(const DecodeArgs& a, int gq, void* stream);
 int launch_export(const ExportArgs& a, void* stream);
 int launch_merge(const MergeArgs& a, void* stream);
 int launch_dgap(const struct DgapArgs& a, int batch, void* stream);

@@ -70,8 +70,12 @@ CASES = [
     (W("k4v4_gq8_g64", 1, 64, 8, 900, 4, 4, gk=64), 5),
     (W("k8v8_gq4", 1, 32, 8, 700, 8, 8), 12),
     (W("k1v2_gq4_g128", 1, 32, 8, 1500, 1, 2, gk=128), 24),
-    (W("k1v1_gq1_vector", 1, 8, 8, 500, 1, 1), 8),                   # vector kernel, 8 queries per group
-    (W("k2v2_gq2_vector", 1, 16, 8, 300, 2, 2), 6),                  # vector kernel, 2 queries per group
+    (W("k1v1_gq1_matrix", 1, 8, 8, 500, 1, 1), 8),                   # one head per kv head: 8-query groups
+    (W("k2v2_gq2_matrix", 1, 16, 8, 300, 2, 2), 6),                  # two heads: 2-query groups
+    (W("k1v1_gq1_rows16", 1, 8, 8, 600, 1, 1), 32),                  # 16 queries of one head per group
+    (W("k2v1_gq2_odd", 1, 16, 8, 400, 2, 1), 7),                     # two heads, odd n_q: one query per group
+    (W("k1v1_gq1_g64_vector", 1, 8, 8, 500, 1, 1, gk=64), 8),       # vector kernel, 8 queries per group
+    (W("k2v2_gq2_g64_vector", 1, 16, 8, 300, 2, 2, gk=64), 6),      # vector kernel, 2 queries per group
     (W("k1v4_gq4_vector", 1, 32, 8, 800, 1, 4), 9),                  # vector kernel, 4-row groups
     (W("ragged_mixed_g64", 3, 32, 8, (900, 64, 300), (1, 2, 4), (1, 2, 4), gk=64), 33),
     (W("whole_sequence", 1, 32, 8, 48, 1, 1), 48),                   # n_q = L
