@@ -150,7 +150,8 @@ def cpu_baseline(w):
     return {
         "value": round(nbytes / dt / 1e9, 4),
         "unit": "GB/s",
-        "cores": max(1, min(threads, len(heads))),
+        # the most threads the sample keeps busy at once (the attention phase)
+        "cores": max(threads, max(1, min(threads, len(heads)))),
         "kind": "oracle",
         "sample": (f"one full {L}-token K{bk}V{bv} layer ({w.num_kv_heads} kv heads, {w.num_q_heads} query heads): "
                    f"fp64 dequantization ({len(heads)} independent per-head calls on "
