@@ -389,17 +389,20 @@ def chunk_leg(handles, w, launch_bytes: int, stream, iters: int):
         # QK and PV: 2 * 2 * d flops per (query, head, visible token)
         flops = 4 * w.head_dim * w.num_q_heads * w.batch * sum(L - n_q + 1 + i for i in range(n_q))
         gq = w.group_q
-        # the row groups the library forms (K1V1, value groups of 32): 16 rows
-        # when whole queries fill them, else 8 or the query heads of a kv head
-        rows = 16 if 16 % gq == 0 and n_q % (16 // gq) == 0 else 8 if (gq == 4 and n_q % 2 == 0) or gq == 8 else gq
+        # the row groups the library forms (K1V1, value groups of 32): 32 or
+        # 16 rows when whole queries fill them, else 8 or the query heads of a
+        # kv head
+        rows = next((r for r in (32, 16) if r % gq == 0 and n_q % (r // gq) == 0),
+                    8 if (gq == 4 and n_q % 2 == 0) or gq == 8 else gq)
         out["us_per_layer"].append(round(us, 3))
         out["query_tokens_per_s_per_layer"].append(round(n_q * w.batch / (us * 1e-6), 1))
         out["cache_gbs_one_pass"].append(round(launch_bytes / (us * 1e-6) / 1e9, 2))
         out["useful_tflops"].append(round(flops / (us * 1e-6) / 1e12, 2))
         out["row_groups_per_kv_head"].append(n_q * gq // rows)
         del q, o, ws
-    out["note"] = ("each row group of up to 16 (query, head) rows is one pass over the kv head's cache "
-                   "(the 16-row chunk kernel); the useful flops count each visible (query, head, token) once")
+    out["note"] = ("each row group of up to 32 (query, head) rows is one pass over the kv head's cache "
+                   "(the chunk kernel: two row halves of 16 share each unpacked code operand); the useful flops "
+                   "count each visible (query, head, token) once")
     # the matrix-core roofline of the contraction (fp16 operands, fp32 accumulation)
     out["roofline"] = {"bound": "mfma", "peak": MFMA_FP16_PEAK_TFLOPS, "unit": "TFLOP/s",
                        "frac": [round(t / MFMA_FP16_PEAK_TFLOPS, 4) for t in out["useful_tflops"]]}

@@ -1,4 +1,4 @@
-// Matrix-core chunk attention over 16 (query, head) rows of one kv head.
+// Matrix-core chunk attention over 16 or 32 (query, head) rows of one kv head.
 //
 // Chunk queries (the last n_q cached tokens attend causally over the cache:
 // the decoder's own attention, softmax(q K^T / sqrt(d)) V, applied to several
@@ -27,7 +27,10 @@
 // LDS, since each lane's rows need the scales of all groups.  Per 32-token
 // block and wave: 16 score MFMAs, 2 zero-point MFMAs, 8 value MFMAs for 16
 // rows, against 24 for 8 rows (with half of their value columns unused) in
-// the decode kernel's eight-head layout.
+// the decode kernel's eight-head layout.  A workgroup of 32 rows runs two
+// row halves of 16 over the same blocks: every unpacked key and value
+// operand then feeds both halves' MFMAs, so the unpacking (one vector
+// instruction per operand dword) is paid once per 32 rows.
 #include <hip/hip_runtime.h>
 
 #include "decode_common.h"
@@ -41,28 +44,33 @@ namespace {
 using namespace dec;
 using namespace mfma_ops;
 
-constexpr int kRows = 16;           // rows of a row group
+constexpr int kRows = 16;           // rows of one row half (the M dimension of an MFMA)
 constexpr float kMargin = 6.f;      // lazy softmax reference headroom (log2 units)
 constexpr int kQR = 68;             // dwords per Q' row (64 + 4: rows start in distinct bank quads)
 constexpr int kPR = 36;             // floats per weight row (32 + 4)
 constexpr int kZG = 16;             // key groups per zero-point table
 
-// LDS areas (bytes).  The first holds the cross-wave reduction after the
-// loop, or the staged query rows of the fp16-tail splits (per wave).
+// LDS areas (bytes) of a workgroup of NU row halves (16 * NU rows).  The
+// first holds the cross-wave reduction after the loop, or the staged query
+// rows of the fp16-tail splits (per wave).
 constexpr int kTailQ = kHeadDim * 8;  // floats of one wave's staged query rows (8 rows)
-constexpr int kOffQA = 0;
-constexpr int kBytesQA = (int)sizeof(Reduce<8>);  // the reduction takes 8 rows at a time
-constexpr int kOffPL = (kOffQA + kBytesQA + 15) / 16 * 16;
-constexpr int kOffVM = kOffPL + kWaves * kRows * kPR * 4;
-constexpr int kOffKS = kOffVM + kWaves * 128 * 4;
-constexpr int kOffDZ = kOffKS + kWaves * 64 * 4;
-constexpr int kOffQQ = kOffDZ + kWaves * kZG * kRows * 4;
-constexpr int kOffCS = kOffQQ + kRows * kQR * 4;
-constexpr int kOffVT = kOffCS + kRows * 4;
-constexpr int kSmemBytes = kOffVT + ValueTable2::kWords * 4;
-static_assert(kWaves * kTailQ * 4 <= kBytesQA, "the tail splits' query rows fit the first area");
-static_assert(32 * 8 <= kRows * kPR, "a tail half's weights fit its wave's weight area");
-static_assert(sizeof(Reduce<8>) <= kBytesQA, "8 rows of the reduction fit the first area");
+template <int NU>
+struct ChunkSmem {
+  static constexpr int R = kRows * NU;
+  static constexpr int kOffQA = 0;
+  static constexpr int kBytesQA = (int)sizeof(Reduce<8>);  // the reduction takes 8 rows at a time
+  static constexpr int kOffPL = (kOffQA + kBytesQA + 15) / 16 * 16;
+  static constexpr int kOffVM = kOffPL + kWaves * R * kPR * 4;
+  static constexpr int kOffKS = kOffVM + kWaves * 128 * 4;
+  static constexpr int kOffDZ = kOffKS + kWaves * 64 * 4;
+  static constexpr int kOffQQ = kOffDZ + kWaves * kZG * R * 4;
+  static constexpr int kOffCS = kOffQQ + R * kQR * 4;
+  static constexpr int kOffLM = kOffCS + R * 4;
+  static constexpr int kOffVT = kOffLM + R * 4;
+  static constexpr int kBytes = kOffVT + ValueTable2::kWords * 4;
+  static_assert(kWaves * kTailQ * 4 <= kBytesQA, "the tail splits' query rows fit the first area");
+  static_assert(32 * 8 <= R * kPR, "a tail half's weights fit its wave's weight area");
+};
 
 // Everything one 32-token block reads from memory.
 template <int BK, int BV>
@@ -73,26 +81,31 @@ struct ChunkBlock {
   uint2 vm;            // bytes 8*lane .. 8*lane + 7 of the block's value meta (staged in LDS)
 };
 
-template <int BK, int BV>
+template <int BK, int BV, int NU>
 struct ChunkOcc {  // waves per SIMD (registers), shared with the host's split plan
-  static constexpr int value = chunk_waves(BK, BV);
+  static constexpr int value = chunk_waves(BK, BV, kRows * NU);
 };
 
-template <int BK, int BV, int BPG, bool PAGED>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ChunkOcc<BK, BV>::value))) void
+// NU row halves of 16 rows share every unpacked code operand: each key and
+// value operand feeds NU products (two row halves halve the unpacking per
+// row), the Q' and weight work stays per row.
+template <int BK, int BV, int BPG, bool PAGED, int NU>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(ChunkOcc<BK, BV, NU>::value))) void
 chunk_mfma_kernel(DecodeArgs a) {
-  constexpr int R = kRows;
+  using SM = ChunkSmem<NU>;
+  constexpr int R = SM::R;
   constexpr bool kPairW = BV == 1;  // 1-bit value operands carry pair weights 2^t
-  __shared__ __attribute__((aligned(16))) uint8_t smem[kSmemBytes];
-  uint32_t* const qa_all = reinterpret_cast<uint32_t*>(smem + kOffQA);
-  float* const pl_all = reinterpret_cast<float*>(smem + kOffPL);
-  uint32_t* const vm_all = reinterpret_cast<uint32_t*>(smem + kOffVM);
-  float* const dz_all = reinterpret_cast<float*>(smem + kOffDZ);
-  uint32_t* const qq_s = reinterpret_cast<uint32_t*>(smem + kOffQQ);
-  float* const cs_s = reinterpret_cast<float*>(smem + kOffCS);
-  uint32_t* const vtab = reinterpret_cast<uint32_t*>(smem + kOffVT);
-  uint32_t* const ks_all = reinterpret_cast<uint32_t*>(smem + kOffKS);
-  Reduce<8>& red = *reinterpret_cast<Reduce<8>*>(smem + kOffQA);
+  __shared__ __attribute__((aligned(16))) uint8_t smem[SM::kBytes];
+  uint32_t* const qa_all = reinterpret_cast<uint32_t*>(smem + SM::kOffQA);
+  float* const pl_all = reinterpret_cast<float*>(smem + SM::kOffPL);
+  uint32_t* const vm_all = reinterpret_cast<uint32_t*>(smem + SM::kOffVM);
+  float* const dz_all = reinterpret_cast<float*>(smem + SM::kOffDZ);
+  uint32_t* const qq_s = reinterpret_cast<uint32_t*>(smem + SM::kOffQQ);
+  float* const cs_s = reinterpret_cast<float*>(smem + SM::kOffCS);
+  uint32_t* const vtab = reinterpret_cast<uint32_t*>(smem + SM::kOffVT);
+  uint32_t* const ks_all = reinterpret_cast<uint32_t*>(smem + SM::kOffKS);
+  int* const lim_s = reinterpret_cast<int*>(smem + SM::kOffLM);
+  Reduce<8>& red = *reinterpret_cast<Reduce<8>*>(smem + SM::kOffQA);
 
   const Work wk = find_work<true>(a);
   const DecodeSeq& S = a.seq[wk.si];
@@ -101,9 +114,9 @@ chunk_mfma_kernel(DecodeArgs a) {
   uint32_t vbound = __builtin_amdgcn_raw_buffer_load_b32(head_rsrc(blk + a.vb, 4), 0, 0, 0);
   asm volatile("" ::: "memory");
 
-  if (wk.sp >= S.nq) {  // fp16 tail tokens: the vector path, in two halves of 8 rows
+  if (wk.sp >= S.nq) {  // fp16 tail tokens: the vector path, in parts of 8 rows
     uint32_t* qa = qa_all + wv * kTailQ;
-    for (int half = 0; half < 2; ++half) {
+    for (int half = 0; half < 2 * NU; ++half) {
       float qs0[8], qs1[8];
       load_q_scaled<8, true>(a, S, wk.h, wk.rg, lane, qs0, qs1, 8 * half);
       State<8> st;
@@ -114,7 +127,7 @@ chunk_mfma_kernel(DecodeArgs a) {
       stage_state<8>(st, red, lane, wv);
       __syncthreads();
       write_record<8, true>(a, S, wk.h, wk.rg, wk.sp, red, 8 * half);
-      __syncthreads();  // the reduction is read before the next half's query overlays it
+      __syncthreads();  // the reduction is read before the next part's query overlays it
     }
     return;
   }
@@ -243,34 +256,34 @@ chunk_mfma_kernel(DecodeArgs a) {
     frexpf(mx, &e);
     const float inv = ldexpf(1.f, -e);
     qq_s[g * kQR + lane] = h2u((h2_t){(_Float16)(q0 * inv), (_Float16)(q1 * inv)});
-    if (lane == 0) cs_s[g] = ldexpf(a.qscale, e - CodeUnit<BK>::value);
+    if (lane == 0) {
+      cs_s[g] = ldexpf(a.qscale, e - CodeUnit<BK>::value);
+      lim_s[g] = row_limit(a, S, wk.rg, g);
+    }
   }
   if constexpr (kTabLoads > 0) {
     if ((int)threadIdx.x < kTabLoads) reinterpret_cast<u4_t*>(vtab)[threadIdx.x] = tabw;
   }
   __syncthreads();
-  // q~ of row col in the A layout of the score product (channels 32*kb +
-  // 8*row + e), with the key operand's pair weights: element pair t of a
+  // q~ of row 16u + col in the A layout of the score product (channels 32*kb
+  // + 8*row + e), with the key operand's pair weights: element pair t of a
   // 1-bit operand carries 2^t, odd pairs of a 2-bit operand 4
-  h8_t qa[4];
+  h8_t qa[NU][4];
 #pragma unroll
-  for (int kb = 0; kb < 4; ++kb) {
-    const u4_t v = *reinterpret_cast<const u4_t*>(&qq_s[col * kQR + 16 * kb + 4 * row]);
-    u4_t w;
+  for (int u = 0; u < NU; ++u)
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const _Float16 f = (_Float16)(BK == 1 ? ldexpf(1.f, -t) : (BK == 2 && (t & 1)) ? 0.25f : 1.f);
-      w[t] = h2u(u2h(v[t]) * (h2_t){f, f});
+    for (int kb = 0; kb < 4; ++kb) {
+      const u4_t v = *reinterpret_cast<const u4_t*>(&qq_s[(kRows * u + col) * kQR + 16 * kb + 4 * row]);
+      u4_t w;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const _Float16 f = (_Float16)(BK == 1 ? ldexpf(1.f, -t) : (BK == 2 && (t & 1)) ? 0.25f : 1.f);
+        w[t] = h2u(u2h(v[t]) * (h2_t){f, f});
+      }
+      qa[u][kb] = __builtin_bit_cast(h8_t, w);
     }
-    qa[kb] = __builtin_bit_cast(h8_t, w);
-  }
-  float cs[4];
-  int lim[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    cs[r] = cs_s[4 * row + r];
-    lim[r] = row_limit(a, S, wk.rg, 4 * row + r);
-  }
+  // the score scale and the token limit of rows 16u + 4*row + r stay in LDS
+  // (cs_s, lim_s) and are read per block: registers are scarce at 32 rows
   const int glim = group_limit(a, S, wk.rg);
 
   uint32_t* const ks = ks_all + wv * 64;
@@ -279,15 +292,22 @@ chunk_mfma_kernel(DecodeArgs a) {
   float* const dzt = dz_all + wv * kZG * R;
 
   // zero-point terms sum_c z[c] q~[row][c] of 16 key groups: D[group][row]
-  // (A = z of group col, B = q~ of row col), scaled like the code products
+  // (A = z of group col, B = q~ of row 16u + col), scaled like the code
+  // products
   auto fill_dz = [&](const h8_t (&z)[4]) {
-    f4_t t = {0.f, 0.f, 0.f, 0.f};
+    f4_t t[NU];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-      t = mfma(z[kb], *reinterpret_cast<const h8_t*>(&qq_s[col * kQR + 16 * kb + 4 * row]), t);
+    for (int u = 0; u < NU; ++u) {
+      t[u] = (f4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+        t[u] = mfma(z[kb], *reinterpret_cast<const h8_t*>(&qq_s[(kRows * u + col) * kQR + 16 * kb + 4 * row]), t[u]);
+    }
     wave_lds_sync();  // earlier reads of the table are done
 #pragma unroll
-    for (int r = 0; r < 4; ++r) dzt[(4 * row + r) * R + col] = t[r] * ldexpf(1.f, CodeUnit<BK>::value);
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dzt[(4 * row + r) * R + kRows * u + col] = t[u][r] * ldexpf(1.f, CodeUnit<BK>::value);
   };
   if (nblocks > 0) {
     fill_dz(zq);
@@ -328,19 +348,25 @@ chunk_mfma_kernel(DecodeArgs a) {
     vmf[1] = lane < 32 ? (h2_t){f1, f1} : (h2_t){(_Float16)1.f, (_Float16)1.f};
   }
 
-  // Lane state, rows 4*row + r: the reference m (uniform over the 16 lanes
-  // of the row block) and the lane's share of l.
-  float m[4], l[4];
-  f4_t acc[8], zac = {0.f, 0.f, 0.f, 0.f};
+  // Lane state, rows 16u + 4*row + r: the reference m (uniform over the 16
+  // lanes of the row block) and the lane's share of l.
+  float m[NU][4], l[NU][4];
+  f4_t acc[NU][8], zac[NU];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    m[r] = -__builtin_inff();
-    l[r] = 0.f;
+  for (int u = 0; u < NU; ++u) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      m[u][r] = -__builtin_inff();
+      l[u][r] = 0.f;
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[u][t] = (f4_t){0.f, 0.f, 0.f, 0.f};
+    zac[u] = (f4_t){0.f, 0.f, 0.f, 0.f};
   }
-#pragma unroll
-  for (int t = 0; t < 8; ++t) acc[t] = (f4_t){0.f, 0.f, 0.f, 0.f};
 
-  f4_t dz = {0.f, 0.f, 0.f, 0.f};
+  f4_t dz[NU];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) dz[u] = (f4_t){0.f, 0.f, 0.f, 0.f};
   auto process = [&](const ChunkBlock<BK, BV>& cur, int i) {
     if (BPG == 1 || i % BPG == 0) {
       const int k = i / BPG;
@@ -353,47 +379,73 @@ chunk_mfma_kernel(DecodeArgs a) {
       wave_lds_sync();
       ks[lane] = cur.s;
       wave_lds_sync();
-      dz = *reinterpret_cast<const f4_t*>(&dzt[(k % kZG) * R + 4 * row]);
+#pragma unroll
+      for (int u = 0; u < NU; ++u) dz[u] = *reinterpret_cast<const f4_t*>(&dzt[(k % kZG) * R + kRows * u + 4 * row]);
     }
 
-    // scores of token 16*mb + col, rows 4*row + r; Q' = q~ (.) s of each
-    // 32-channel block kb in the A layout, hi and lo parts
-    f4_t d[2] = {dz, dz};
+    // scores of token 16*mb + col, rows 16u + 4*row + r; Q' = q~ (.) s of
+    // each 32-channel block kb in the A layout, hi and lo parts; each
+    // unpacked key operand serves every row half
+    f4_t d[NU][2];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) d[u][0] = d[u][1] = dz[u];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       const u4_t sv = *reinterpret_cast<const u4_t*>(&ks[16 * kb + 4 * row]);
-      const u4_t qv = __builtin_bit_cast(u4_t, qa[kb]);
-      u4_t h, o;
+      h8_t ahi[NU], alo[NU];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const h2_t hi = u2h(qv[t]) * u2h(sv[t]);
-        h[t] = h2u(hi);
-        o[t] = h2u(__builtin_elementwise_fma(u2h(qv[t]), u2h(sv[t]), -hi));
+      for (int u = 0; u < NU; ++u) {
+        const u4_t qv = __builtin_bit_cast(u4_t, qa[u][kb]);
+        u4_t h, o;
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const h2_t hi = u2h(qv[t]) * u2h(sv[t]);
+          h[t] = h2u(hi);
+          o[t] = h2u(__builtin_elementwise_fma(u2h(qv[t]), u2h(sv[t]), -hi));
+        }
+        ahi[u] = __builtin_bit_cast(h8_t, h);
+        alo[u] = __builtin_bit_cast(h8_t, o);
       }
-      const h8_t ahi = __builtin_bit_cast(h8_t, h), alo = __builtin_bit_cast(h8_t, o);
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb) {
         h8_t b;
         if constexpr (BK == 1) b = unpack_bits(cur.kx[mb][0], kb);
         else if constexpr (BK == 2) b = unpack_pairs2(cur.kx[mb][kb >> 1], kb & 1);
         else b = whole8<BK>(&cur.kx[mb][(BK / 4) * kb]);
-        d[mb] = mfma(ahi, b, d[mb]);
-        d[mb] = mfma(alo, b, d[mb]);
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+          d[u][mb] = mfma(ahi[u], b, d[u][mb]);
+          d[u][mb] = mfma(alo[u], b, d[u][mb]);
+        }
       }
     }
     const int tok = (j0 + kWaves * (i / BPG)) * a.gk + (i % BPG) * 32;
     const bool masked = tok + 32 > glim;
-    float raw[4][2];
+    float raw[NU][4][2];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) raw[r][mb] = d[mb][r];
-    if (masked) {
+    for (int u = 0; u < NU; ++u)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-          if (tok + 16 * mb + col >= lim[r]) raw[r][mb] = -__builtin_inff();
+        for (int mb = 0; mb < 2; ++mb) raw[u][r][mb] = d[u][mb][r];
+    if (masked) {
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const int4 lim = *reinterpret_cast<const int4*>(&lim_s[kRows * u + 4 * row]);
+        const int lr[4] = {lim.x, lim.y, lim.z, lim.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+            if (tok + 16 * mb + col >= lr[r]) raw[u][r][mb] = -__builtin_inff();
+      }
+    }
+    float cs[NU][4];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const f4_t c4 = *reinterpret_cast<const f4_t*>(&cs_s[kRows * u + 4 * row]);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[u][r] = c4[r];
     }
 
     // online softmax (base 2) per row, lazy reference as in the decode
@@ -401,87 +453,108 @@ chunk_mfma_kernel(DecodeArgs a) {
     // those rows moves its reference
     const float ninf = -__builtin_inff();
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float bmr = fmaf(fmaxf(raw[r][0], raw[r][1]), cs[r], -pshift);
-      if (__builtin_amdgcn_ballot_w64(bmr > m[r])) {
-        float b = bmr;
-        b = fmaxf(b, dpp_mov<kQuadXor1>(ninf, b));
-        b = fmaxf(b, dpp_mov<kQuadXor2>(ninf, b));
-        b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
-        b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
-        const float mnew = b > m[r] ? b + kMargin : m[r];
-        // a row with no visible token yet keeps m = -inf and factor 1
-        const float alpha = mnew == m[r] ? 1.f : __builtin_amdgcn_exp2f(m[r] - mnew);
-        l[r] *= alpha;
-        m[r] = mnew;
+    for (int u = 0; u < NU; ++u)
 #pragma unroll
-        for (int t = 0; t < 8; ++t) acc[t][r] *= alpha;
-        zac[r] *= alpha;
+      for (int r = 0; r < 4; ++r) {
+        const float bmr = fmaf(fmaxf(raw[u][r][0], raw[u][r][1]), cs[u][r], -pshift);
+        if (__builtin_amdgcn_ballot_w64(bmr > m[u][r])) {
+          float b = bmr;
+          b = fmaxf(b, dpp_mov<kQuadXor1>(ninf, b));
+          b = fmaxf(b, dpp_mov<kQuadXor2>(ninf, b));
+          b = fmaxf(b, dpp_mov<kHalfMirror>(ninf, b));
+          b = fmaxf(b, dpp_mov<kMirror>(ninf, b));
+          const float mnew = b > m[u][r] ? b + kMargin : m[u][r];
+          // a row with no visible token yet keeps m = -inf and factor 1
+          const float alpha = mnew == m[u][r] ? 1.f : __builtin_amdgcn_exp2f(m[u][r] - mnew);
+          l[u][r] *= alpha;
+          m[u][r] = mnew;
+#pragma unroll
+          for (int t = 0; t < 8; ++t) acc[u][t][r] *= alpha;
+          zac[u][r] *= alpha;
+        }
       }
-    }
-    float e[4][2];
+    float e[NU][4][2];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb) e[r][mb] = __builtin_amdgcn_exp2f(fmaf(raw[r][mb], cs[r], -m[r]));
-    if (masked) {  // masked tokens weigh 0, also while m is still -inf
+    for (int u = 0; u < NU; ++u)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) e[r][mb] = raw[r][mb] == -__builtin_inff() ? 0.f : e[r][mb];
+        for (int mb = 0; mb < 2; ++mb)
+          e[u][r][mb] = __builtin_amdgcn_exp2f(fmaf(raw[u][r][mb], cs[u][r], -m[u][r]));
+    if (masked) {  // masked tokens weigh 0, also while m is still -inf
+#pragma unroll
+      for (int u = 0; u < NU; ++u)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb) e[u][r][mb] = raw[u][r][mb] == -__builtin_inff() ? 0.f : e[u][r][mb];
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) l[r] += e[r][0] + e[r][1];
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) l[u][r] += e[u][r][0] + e[u][r][1];
 
-    // weights to the A layout (lane: row col, tokens of K-group row), and
-    // the block's value meta to LDS
+    // weights to the A layout (lane: row 16u + col, tokens of K-group row),
+    // and the block's value meta to LDS
     wave_lds_sync();
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      pl[(4 * row + r) * kPR + col] = e[r][0];
-      pl[(4 * row + r) * kPR + 16 + col] = e[r][1];
-    }
+    for (int u = 0; u < NU; ++u)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pl[(kRows * u + 4 * row + r) * kPR + col] = e[u][r][0];
+        pl[(kRows * u + 4 * row + r) * kPR + 16 + col] = e[u][r][1];
+      }
     *reinterpret_cast<uint2*>(&vml[2 * lane]) = make_uint2(h2u(u2h(cur.vm.x) * vmf[0]), h2u(u2h(cur.vm.y) * vmf[1]));
     wave_lds_sync();
-    const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[col * kPR + 4 * row]);
-    const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[col * kPR + 16 + 4 * row]);
-    const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
     // p in fp16 hi + lo parts
-    u4_t phi, plo;
+    u4_t phi[NU], plo[NU];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      float f0 = p[2 * t], f1 = p[2 * t + 1];
-      keep_f32(f0, f1);
-      uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});
-      asm("" : "+v"(hw));
-      const h2_t hi = u2h(hw);
-      float g0 = fmaf(p[2 * t], 1.f, -(float)hi.x), g1 = fmaf(p[2 * t + 1], 1.f, -(float)hi.y);
-      keep_f32(g0, g1);
-      phi[t] = hw;
-      plo[t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
+    for (int u = 0; u < NU; ++u) {
+      const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[(kRows * u + col) * kPR + 4 * row]);
+      const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[(kRows * u + col) * kPR + 16 + 4 * row]);
+      const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float f0 = p[2 * t], f1 = p[2 * t + 1];
+        keep_f32(f0, f1);
+        uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});
+        asm("" : "+v"(hw));
+        const h2_t hi = u2h(hw);
+        float g0 = fmaf(p[2 * t], 1.f, -(float)hi.x), g1 = fmaf(p[2 * t + 1], 1.f, -(float)hi.y);
+        keep_f32(g0, g1);
+        phi[u][t] = hw;
+        plo[u][t] = h2u((h2_t){(_Float16)g0, (_Float16)g1});
+      }
     }
     // zero-point terms: B = the staged zeros of group col (columns past the
     // groups: zero)
     {
       u4_t zb = {0u, 0u, 0u, 0u};
       if (col < ng) zb = *reinterpret_cast<const u4_t*>(&vml[16 * ng + 16 * col + 4 * row]);
-      zac = mfma(__builtin_bit_cast(h8_t, phi), __builtin_bit_cast(h8_t, zb), zac);
-      zac = mfma(__builtin_bit_cast(h8_t, plo), __builtin_bit_cast(h8_t, zb), zac);
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        zac[u] = mfma(__builtin_bit_cast(h8_t, phi[u]), __builtin_bit_cast(h8_t, zb), zac[u]);
+        zac[u] = mfma(__builtin_bit_cast(h8_t, plo[u]), __builtin_bit_cast(h8_t, zb), zac[u]);
+      }
     }
     // P'_g = p * s_v of each value group (32 channels: tiles 2g, 2g + 1), and
-    // the products of its tiles
-    h8_t pg;
+    // the products of its tiles; each unpacked value operand serves every
+    // row half
+    h8_t pg[NU];
 #pragma unroll
     for (int mb = 0; mb < 8; ++mb) {
       if (mb % 2 == 0) {
         const u4_t sg = *reinterpret_cast<const u4_t*>(&vml[16 * (mb / 2) + 4 * row]);
-        u4_t w;
 #pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          const h2_t s2 = u2h(sg[t]);
-          w[t] = h2u(__builtin_elementwise_fma(u2h(phi[t]), s2, u2h(plo[t]) * s2));
+        for (int u = 0; u < NU; ++u) {
+          u4_t w;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const h2_t s2 = u2h(sg[t]);
+            w[t] = h2u(__builtin_elementwise_fma(u2h(phi[u][t]), s2, u2h(plo[u][t]) * s2));
+          }
+          pg[u] = __builtin_bit_cast(h8_t, w);
         }
-        pg = __builtin_bit_cast(h8_t, w);
       }
       h8_t bv;
       if constexpr (BV == 1) {
@@ -494,7 +567,8 @@ chunk_mfma_kernel(DecodeArgs a) {
       } else {
         bv = whole8<BV>(&cur.vx[(BV / 4) * mb]);
       }
-      acc[mb] = mfma(pg, bv, acc[mb]);
+#pragma unroll
+      for (int u = 0; u < NU; ++u) acc[u][mb] = mfma(pg[u], bv, acc[u][mb]);
     }
   };
 
@@ -514,72 +588,89 @@ chunk_mfma_kernel(DecodeArgs a) {
   const int ln = __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
   const int ecol = ln & 15, erow = ln >> 4;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    l[r] += dpp_mov<kQuadXor1>(0.f, l[r]);
-    l[r] += dpp_mov<kQuadXor2>(0.f, l[r]);
-    l[r] += dpp_mov<kHalfMirror>(0.f, l[r]);
-    l[r] += dpp_mov<kMirror>(0.f, l[r]);
-  }
+  for (int u = 0; u < NU; ++u)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      l[u][r] += dpp_mov<kQuadXor1>(0.f, l[u][r]);
+      l[u][r] += dpp_mov<kQuadXor2>(0.f, l[u][r]);
+      l[u][r] += dpp_mov<kHalfMirror>(0.f, l[u][r]);
+      l[u][r] += dpp_mov<kMirror>(0.f, l[u][r]);
+    }
   const float kAccScale = ldexpf(1.f, (BV == 2 ? 0 : -CodeUnit<BV>::value) - xshift);
-  float zg[4][4];  // zero-point terms of rows 4*erow + r, group g, in this lane
+  // rows 8*part .. 8*part + 7 (row half part / 2, lane row blocks 2*(part %
+  // 2), 2*(part % 2) + 1) pass through the reduction area one part after
+  // the other
 #pragma unroll
-  for (int g = 0; g < 4; ++g)
+  for (int u = 0; u < NU; ++u) {
+    float zg[4][4];  // zero-point terms of rows 16u + 4*erow + r, group g, in this lane
 #pragma unroll
-    for (int r = 0; r < 4; ++r) zg[g][r] = __shfl(zac[r], 16 * erow + g);
-  // rows 8*half .. 8*half + 7 (lane row blocks 2*half, 2*half + 1) pass
-  // through the reduction area one half after the other
-  for (int half = 0; half < 2; ++half) {
-    __syncthreads();  // the area is free
-    if ((erow >> 1) == half) {
-      const int rb = erow & 1;
+    for (int g = 0; g < 4; ++g)
 #pragma unroll
-      for (int mb = 0; mb < 8; ++mb)
+      for (int r = 0; r < 4; ++r) zg[g][r] = __shfl(zac[u][r], 16 * erow + g);
+    for (int half = 0; half < 2; ++half) {
+      __syncthreads();  // the area is free
+      if ((erow >> 1) == half) {
+        const int rb = erow & 1;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          red.acc[wv][(4 * rb + r) * kHeadDim + 16 * mb + ecol] = acc[mb][r] * kAccScale + zg[mb / 2][r];
-      if (ecol == 0) {
+        for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          red.m[wv][4 * rb + r] = m[r];
-          red.l[wv][4 * rb + r] = l[r];
+          for (int r = 0; r < 4; ++r)
+            red.acc[wv][(4 * rb + r) * kHeadDim + 16 * mb + ecol] = acc[u][mb][r] * kAccScale + zg[mb / 2][r];
+        if (ecol == 0) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            red.m[wv][4 * rb + r] = m[u][r];
+            red.l[wv][4 * rb + r] = l[u][r];
+          }
         }
       }
+      __syncthreads();
+      write_record<8, true>(a, S, wk.h, wk.rg, wk.sp, red, kRows * u + 8 * half);
     }
-    __syncthreads();
-    write_record<8, true>(a, S, wk.h, wk.rg, wk.sp, red, 8 * half);
   }
 }
 
-template <int BK, int BV, int BPG>
+template <int BK, int BV, int BPG, int NU>
 int launch_p(const DecodeArgs& a, void* stream) {
   if (a.pm.table != nullptr)
-    hipLaunchKernelGGL((chunk_mfma_kernel<BK, BV, BPG, true>), dim3(a.total_wg), dim3(64 * kWaves), 0,
+    hipLaunchKernelGGL((chunk_mfma_kernel<BK, BV, BPG, true, NU>), dim3(a.total_wg), dim3(64 * kWaves), 0,
                        (hipStream_t)stream, a);
   else
-    hipLaunchKernelGGL((chunk_mfma_kernel<BK, BV, BPG, false>), dim3(a.total_wg), dim3(64 * kWaves), 0,
+    hipLaunchKernelGGL((chunk_mfma_kernel<BK, BV, BPG, false, NU>), dim3(a.total_wg), dim3(64 * kWaves), 0,
                        (hipStream_t)stream, a);
   return (int)hipGetLastError();
 }
 
-template <int BK, int BV>
+template <int BK, int BV, int NU>
 int launch_g(const DecodeArgs& a, void* stream) {
   switch (a.gk / 32) {
-    case 1: return launch_p<BK, BV, 1>(a, stream);
-    case 2: return launch_p<BK, BV, 2>(a, stream);
-    case 4: return launch_p<BK, BV, 4>(a, stream);
+    case 1: return launch_p<BK, BV, 1, NU>(a, stream);
+    case 2: return launch_p<BK, BV, 2, NU>(a, stream);
+    case 4: return launch_p<BK, BV, 4, NU>(a, stream);
     default: return (int)hipErrorInvalidValue;
   }
 }
 
+// 32 rows for 1- and 2-bit classes (the 4-bit blocks leave too few
+// registers for two row halves), 16 rows for all.
+template <int BK, int BV>
+int launch_r(const DecodeArgs& a, int rows, void* stream) {
+  if constexpr (chunk_rows32(BK, BV)) {
+    if (rows == 32) return launch_g<BK, BV, 2>(a, stream);
+  }
+  if (rows == 16) return launch_g<BK, BV, 1>(a, stream);
+  return (int)hipErrorInvalidValue;
+}
+
 }  // namespace
 
-int launch_chunk_matrix(const DecodeArgs& a, int bk, int bv, void* stream) {
+int launch_chunk_matrix(const DecodeArgs& a, int bk, int bv, int rows, void* stream) {
   if (a.total_wg <= 0) return 0;
-  if (bk == 1 && bv == 1) return launch_g<1, 1>(a, stream);
-  if (bk == 1 && bv == 2) return launch_g<1, 2>(a, stream);
-  if (bk == 2 && bv == 1) return launch_g<2, 1>(a, stream);
-  if (bk == 2 && bv == 2) return launch_g<2, 2>(a, stream);
-  if (bk == 4 && bv == 4) return launch_g<4, 4>(a, stream);
+  if (bk == 1 && bv == 1) return launch_r<1, 1>(a, rows, stream);
+  if (bk == 1 && bv == 2) return launch_r<1, 2>(a, rows, stream);
+  if (bk == 2 && bv == 1) return launch_r<2, 1>(a, rows, stream);
+  if (bk == 2 && bv == 2) return launch_r<2, 2>(a, rows, stream);
+  if (bk == 4 && bv == 4) return launch_r<4, 4>(a, rows, stream);
   return (int)hipErrorInvalidValue;  // 8-bit classes take the decode kernel's row groups
 }
 

@@ -498,23 +498,24 @@ struct Rows {
 };
 
 // Single-token decode: one row group of the kv head's query heads.  Chunk
-// queries: the largest row group a kernel has (matrix: 16 rows in the chunk
-// kernel for 1-, 2- and 4-bit classes with value groups of 32 channels, 4,
-// 5, 8 in the decode kernel; vector: also 1, 2) made of whole queries, with
-// a whole number of groups.
+// queries: the largest row group a kernel has (matrix: 32 rows in the chunk
+// kernel for 1- and 2-bit classes, 16 for those and 4-bit classes, with
+// value groups of 32 channels; 4, 5, 8 in the decode kernel; vector: also
+// 1, 2) made of whole queries, with a whole number of groups.
 Rows rows_for(const kvq_cache* c, bool matrix, int nqry, int bk, int bv) {
   const int gqh = c->d.num_q_heads / c->d.num_kv_heads;
   Rows r;
   r.rows = gqh;
   if (nqry <= 1) return r;
-  static const int kMatrixRows[] = {16, 8, 5, 4}, kVectorRows[] = {8, 5, 4, 2, 1};
+  static const int kMatrixRows[] = {32, 16, 8, 5, 4}, kVectorRows[] = {8, 5, 4, 2, 1};
   const int* cand = matrix ? kMatrixRows : kVectorRows;
-  const int ncand = matrix ? 4 : 5;
+  const int ncand = 5;
   const bool rows16 = matrix && c->d.value_group == 32 && bk + bv <= 8;
   r.nqry = nqry;
   for (int k = 0; k < ncand; ++k) {
     const int rg = cand[k];
-    if (rg == 16 && !rows16) continue;
+    if (rg >= 16 && !rows16) continue;
+    if (rg == 32 && !kvq::chunk_rows32(bk, bv)) continue;
     if (rg % gqh == 0 && nqry % (rg / gqh) == 0) {
       r.qpr = rg / gqh;
       r.nrg = nqry / r.qpr;
@@ -597,7 +598,7 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.qscale = qscale;
     const Rows r = rows_for(c, c->matrix[cls.second[0]] != 0, p.nqry, cls.first.first, cls.first.second);
     a.nqry = r.nqry; a.qpr = r.qpr; a.nrg = r.nrg; a.gqh = d.num_q_heads / d.num_kv_heads;
-    for (int g = 0; g < 16; ++g) {
+    for (int g = 0; g < 32; ++g) {
       a.row_x[g] = g / a.gqh;
       a.row_off[g] = a.row_x[g] * d.num_q_heads + g % a.gqh;
     }
@@ -620,7 +621,7 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.nseq = n;
     a.total_wg = wg;
     const int e = !c->matrix[cls.second[0]] ? kvq::launch_decode(a, cls.first.first, cls.first.second, r.rows, stream)
-                  : r.rows == 16       ? kvq::launch_chunk_matrix(a, cls.first.first, cls.first.second, stream)
+                  : r.rows >= 16 ? kvq::launch_chunk_matrix(a, cls.first.first, cls.first.second, r.rows, stream)
                                        : kvq::launch_decode_matrix(a, cls.first.first, cls.first.second, r.rows, stream);
     if (e) return hip_fail(e, "decode launch");
   }

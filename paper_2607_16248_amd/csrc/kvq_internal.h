@@ -162,7 +162,7 @@ struct DecodeArgs {
   // row g of a row group is chunk query rg*qpr + row_x[g] and head
   // h*gqh + (row_off[g] - row_x[g]*Hq): row_off[g] = row_x[g]*Hq + g % gqh
   // (host-computed, so the kernels divide nothing)
-  int32_t row_off[16], row_x[16];
+  int32_t row_off[32], row_x[32];
   PageMap pm;
 };
 
@@ -248,8 +248,8 @@ bool matrix_decode_supported(int bk, int bv, int gq, int gk, int gv, uint64_t he
 // Waves per SIMD of the matrix-core kernel for this bit class (2, 3 or 4);
 // the vector kernel runs two.
 int matrix_decode_occupancy(int bk, int bv, int gk, int gq);
-// Chunk queries over 16-row groups (chunk_mfma.hip).
-int launch_chunk_matrix(const DecodeArgs& a, int bk, int bv, void* stream);
+// Chunk queries over row groups of 16 or 32 rows (chunk_mfma.hip).
+int launch_chunk_matrix(const DecodeArgs& a, int bk, int bv, int rows, void* stream);
 // The matrix-core decode kernels of one bit class (decode_mfma.hip, one
 // object per class); launch_decode_matrix (matrix_dispatch.cpp) picks one.
 template <int BK, int BV>

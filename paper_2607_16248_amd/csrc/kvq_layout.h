@@ -67,11 +67,14 @@ KVQ_HD constexpr bool matrix_heads(int gq, int gk) {
 // and values with one 32-token block per key group, three for the other 1-
 // and 2-bit four-head cases with one block per group, else two (registers).
 // bpg = key_group / 32.
-// gq = 16 names the 16-row chunk kernel: three waves per SIMD for 1-bit
-// values with 1- or 2-bit keys, else two.
-KVQ_HD constexpr int chunk_waves(int bk, int bv) { return (bv == 1 && bk <= 2) ? 3 : 2; }
+// gq = 16 or 32 names the chunk kernel with that many rows: three waves per
+// SIMD for 16 rows of 1-bit values with 1- or 2-bit keys, else two.
+KVQ_HD constexpr int chunk_waves(int bk, int bv, int rows) { return (rows == 16 && bv == 1 && bk <= 2) ? 3 : 2; }
+// Row groups of 32 (two row halves sharing the unpacked operands) for 1- and
+// 2-bit keys and values.
+KVQ_HD constexpr bool chunk_rows32(int bk, int bv) { return bk <= 2 && bv <= 2; }
 KVQ_HD constexpr int matrix_waves(int bk, int bv, int bpg, int gq) {
-  return gq == 16 ? chunk_waves(bk, bv) : (gq > 4 || bk > 2 || bv > 2) ? 2 : bpg == 1 ? (bk + bv == 2 ? 4 : 3) : 2;
+  return gq >= 16 ? chunk_waves(bk, bv, gq) : (gq > 4 || bk > 2 || bv > 2) ? 2 : bpg == 1 ? (bk + bv == 2 ? 4 : 3) : 2;
 }
 
 KVQ_HD inline int pair_bit(int blk4, int e) {

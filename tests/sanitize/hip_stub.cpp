@@ -44,7 +44,7 @@ int launch_word_reset(const WordReset& r, void*) {
 }
 int launch_decode(const DecodeArgs&, int, int, int, void*) { return ++g_launches, 0; }
 int launch_decode_matrix(const DecodeArgs&, int, int, int, void*) { return ++g_launches, 0; }
-int launch_chunk_matrix(const DecodeArgs&, int, int, void*) { return ++g_launches, 0; }
+int launch_chunk_matrix(const DecodeArgs&, int, int, int, void*) { return ++g_launches, 0; }
 int launch_export(const ExportArgs&, void*) { return ++g_launches, 0; }
 int launch_merge(const MergeArgs&, void*) { return ++g_launches, 0; }
 int launch_dgap(const DgapArgs&, int, void*) { return ++g_launches, 0; }

@@ -64,7 +64,7 @@ def _check(c, q, out, heads=None):
 
 
 CASES = [
-    (W("k1v1_gq4_L1000", 1, 32, 8, 1000, 1, 1), 40),                 # masks inside packed blocks; 8-row groups
+    (W("k1v1_gq4_L1000", 1, 32, 8, 1000, 1, 1), 40),                 # masks inside packed blocks; 32-row groups
     (W("k2v2_gq4_L777_odd", 1, 32, 8, 777, 2, 2), 7),                # odd n_q: 4-row groups
     (W("k2v2_gq5_R128_t3", 2, 40, 8, (600, 333), 2, 2, R=128, dist="student_t3"), 16),  # masks in the fp16 tail
     (W("k4v4_gq8_g64", 1, 64, 8, 900, 4, 4, gk=64), 5),
@@ -72,17 +72,22 @@ CASES = [
     (W("k1v2_gq4_g128", 1, 32, 8, 1500, 1, 2, gk=128), 24),
     (W("k1v1_gq1_matrix", 1, 8, 8, 500, 1, 1), 8),                   # one head per kv head: 8-query groups
     (W("k2v2_gq2_matrix", 1, 16, 8, 300, 2, 2), 6),                  # two heads: 2-query groups
-    (W("k1v1_gq1_rows16", 1, 8, 8, 600, 1, 1), 32),                  # 16 queries of one head per group
+    (W("k1v1_gq1_rows32", 1, 8, 8, 600, 1, 1), 32),                  # 32 queries of one head per group
     (W("k2v1_gq2_odd", 1, 16, 8, 400, 2, 1), 7),                     # two heads, odd n_q: one query per group
     (W("k1v1_gq1_g64_vector", 1, 8, 8, 500, 1, 1, gk=64), 8),       # vector kernel, 8 queries per group
     (W("k2v2_gq2_g64_vector", 1, 16, 8, 300, 2, 2, gk=64), 6),      # vector kernel, 2 queries per group
     (W("k1v4_gq4_vector", 1, 32, 8, 800, 1, 4), 9),                  # vector kernel, 4-row groups
     (W("ragged_mixed_g64", 3, 32, 8, (900, 64, 300), (1, 2, 4), (1, 2, 4), gk=64), 33),
     (W("whole_sequence", 1, 32, 8, 48, 1, 1), 48),                   # n_q = L
-    # 16-row groups (the chunk kernel): 2 queries x 8 heads, and 4 x 4 over
-    # two ragged sequences with 64-token key groups and 1-bit values
+    # the chunk kernel: 16-row groups (2 queries x 8 heads at 4 bits, 4 x 4 at
+    # 1 and 2 bits where 8 queries do not divide n_q) and 32-row groups (two
+    # row halves: 8 x 4 over two ragged sequences with 64-token key groups
+    # and 1-bit values, 4 x 8 heads)
     (W("k4v4_gq8_rows16", 1, 64, 8, 900, 4, 4), 6),
-    (W("k2v1_gq4_rows16_g64", 2, 32, 8, (1000, 517), 2, 1, gk=64), 8),
+    (W("k1v1_gq4_rows16", 1, 32, 8, 700, 1, 1), 4),
+    (W("k2v2_gq4_rows16", 1, 32, 8, 650, 2, 2), 12),
+    (W("k2v1_gq4_rows32_g64", 2, 32, 8, (1000, 517), 2, 1, gk=64), 8),
+    (W("k1v2_gq8_rows32", 1, 64, 8, 700, 1, 2), 4),
 ]
 
 
