@@ -29,8 +29,8 @@
 //     through LDS.  A tile of 16 channels keeps only the columns of its
 //     value group (the rest of its B operand is zero), so tiles of
 //     different groups share one accumulator: two accumulators hold the
-//     128 channels of 4 heads.  (Five heads: the solo quad of head 4 also
-//     carries the residual of P' in its spare columns.)
+//     128 channels of 4 heads.  (Five heads: a second quad carries head 4
+//     alone, in its columns 0-3.)
 //
 // Packed key codes become operands with a shift or two and one AND per
 // element pair: a set bit at mantissa position w of a half is the exact fp16
@@ -629,9 +629,8 @@ decode_mfma_kernel(DecodeArgs a) {
     wave_lds_sync();
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      // Five heads: the second quad carries head 4 alone, with the hi and
-      // lo halves of its P' in columns 0-3 and 4-7 of one MFMA (columns
-      // 8-15 zero) instead of two MFMAs over an almost empty quad.
+      // Five heads: the second quad carries head 4 alone (columns 0-3, the
+      // rest zero).
       const bool solo = GQ == 5 && q == 1;
       const int Hp = solo ? 4 : 4 * q + hc;
       const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[Hp * kPRow + 4 * row]);
@@ -639,22 +638,15 @@ decode_mfma_kernel(DecodeArgs a) {
       const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
 
       // P' = p * s_v rounded once to fp16 (the product is one mixed-precision
-      // fma from the fp32 p and the fp16 scale); the five-head solo quad
-      // also carries the residual in its spare columns
+      // fma from the fp32 p and the fp16 scale, then a round to nearest)
       u4_t bhi;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const h2_t s2 = u2h(cur.sv[t]);
         float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
         keep_f32(f0, f1);
-        uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});  // nearest: the residuals carry both signs
-        asm("" : "+v"(hw));  // the residuals read the packed halves
-        const h2_t hi = u2h(hw);
-        float g0 = fmaf(p[2 * t], (float)s2.x, -(float)hi.x);
-        float g1 = fmaf(p[2 * t + 1], (float)s2.y, -(float)hi.y);
-        keep_f32(g0, g1);
-        const uint32_t lw = h2u((h2_t){(_Float16)g0, (_Float16)g1});
-        bhi[t] = solo ? (hc == 0 ? hw : hc == 1 ? lw : 0u) : hw;
+        const uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});
+        bhi[t] = solo && hc != 0 ? 0u : hw;
         const h2_t z2 = u2h(cur.zv[t]);
         float& za = zacc[q][kPairW ? t : 0];
         za = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, za));
@@ -745,17 +737,13 @@ decode_mfma_kernel(DecodeArgs a) {
     for (int t = 1; t < NZ; ++t) zs = fmaf(zacc[q][t], (float)(1 << t), zs);
     zs += __shfl_xor(zs, 16);
     zs += __shfl_xor(zs, 32);
-    const bool solo = GQ == 5 && q == 1;  // head 4: hi columns 0-3, lo columns 4-7
+    const bool solo = GQ == 5 && q == 1;  // head 4 in columns 0-3
     const int H = solo ? 4 : 4 * q + ehc;
     // accumulator e of column group exc holds tile 2j + e, tile_col(j) = exc
     const int ej = ng == 2 ? 2 * (exc & 1) + (exc >> 1) : exc;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      f4_t v = acc[q][e];
-      if (solo) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] += __shfl_xor(v[i], 4);
-      }
+      const f4_t v = acc[q][e];
       if (solo ? ehc == 0 : H < GQ) {
         const int mb = 2 * ej + e;
 #pragma unroll
