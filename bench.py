@@ -416,16 +416,17 @@ def paged_leg(w, qs, dev, stream, iters: int, nlayers: int = 8):
     """The split kernel over paged caches (pages of PAGE_TOKENS tokens from a
     shared pool, block table per sequence) against contiguous caches holding
     the same seeded tokens: nlayers of each, rotating, HIP events on the
-    launch stream; and the decode outputs of the two compared bit for bit."""
+    launch stream; and the decode outputs of the two compared bit for bit.
+    The two sets are allocated layer by layer in turn, so that both meet the
+    same state of device memory."""
     import torch
 
     from paper_2607_16248_amd import kvq
     from workloads import gen_kv_device
 
-    sets = {}
-    for name, P in (("contiguous", 0), ("paged", PAGE_TOKENS)):
-        cs = []
-        for l in range(nlayers):
+    sets = {"contiguous": [], "paged": []}
+    for l in range(nlayers):
+        for name, P in (("contiguous", 0), ("paged", PAGE_TOKENS)):
             c = kvq.KVCache(w.batch, w.num_q_heads, w.num_kv_heads, max(w.lens), list(w.bits_k), list(w.bits_v),
                             key_group=w.key_group, value_group=w.value_group, fp16_window=w.window, device=dev,
                             page_tokens=P)
@@ -438,8 +439,7 @@ def paged_leg(w, qs, dev, stream, iters: int, nlayers: int = 8):
                 del K, V
             c.append(Kb, Vb, list(w.lens))
             del Kb, Vb
-            cs.append(c)
-        sets[name] = cs
+            sets[name].append(c)
     torch.cuda.synchronize()
     out = {"page_tokens": PAGE_TOKENS, "layers": nlayers}
     outs = {}
