@@ -785,12 +785,10 @@ int launch_t(const DecodeArgs& a, void* stream) {
 template <int BK, int BV, int BPG>
 int launch_gq(const DecodeArgs& a, int gq, void* stream) {
   switch (gq) {
-    case 1:  // one or two query heads per kv head: 32-token key groups only
-      if constexpr (BPG == 1) return launch_t<BK, BV, BPG, 1>(a, stream);
-      return (int)hipErrorInvalidValue;
+    case 1:  // one or two query heads per kv head: the four-head layout with empty heads
+      return launch_t<BK, BV, BPG, 1>(a, stream);
     case 2:
-      if constexpr (BPG == 1) return launch_t<BK, BV, BPG, 2>(a, stream);
-      return (int)hipErrorInvalidValue;
+      return launch_t<BK, BV, BPG, 2>(a, stream);
     case 4: return launch_t<BK, BV, BPG, 4>(a, stream);
     case 5: return launch_t<BK, BV, BPG, 5>(a, stream);
     case 8: return launch_t<BK, BV, BPG, 8>(a, stream);

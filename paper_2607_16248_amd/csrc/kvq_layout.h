@@ -54,14 +54,13 @@ namespace kvq {
 
 // Which caches the matrix-core decode kernel serves: 1- or 2-bit keys and
 // values in any combination, or 4- or 8-bit keys and values in any
-// combination; 4, 5 or 8 query heads per kv head, or 1 or 2 with key groups
-// of 32 tokens (the four-head layout with empty heads); value groups of at
-// least 32 channels.
+// combination; 1, 2, 4, 5 or 8 query heads per kv head (1 and 2 in the
+// four-head layout with empty heads); value groups of at least 32 channels.
 KVQ_HD constexpr bool matrix_bits(int bk, int bv) {
   return ((bk == 1 || bk == 2) && (bv == 1 || bv == 2)) || ((bk == 4 || bk == 8) && (bv == 4 || bv == 8));
 }
 KVQ_HD constexpr bool matrix_heads(int gq, int gk) {
-  return gq == 4 || gq == 5 || gq == 8 || ((gq == 1 || gq == 2) && gk == 32);
+  return (gq == 1 || gq == 2 || gq == 4 || gq == 5 || gq == 8) && gk % 32 == 0;
 }
 // Waves per SIMD its instantiations are compiled for: four for 1-bit keys
 // and values with one 32-token block per key group, three for the other 1-

@@ -6,8 +6,9 @@ seeded, byte-identical cache, through the C ABI.
 - masked tokens inside packed blocks (no fp16 window: the chunk reaches
   into the last key groups), inside the fp16 tail, and n_q = L (the first
   query sees one token: its value row);
-- every row-group shape: matrix kernel with 4, 5 and 8 rows (one or two
-  queries per group), vector kernel with 1, 2, 4 or 8 rows;
+- every row-group shape: the chunk kernel with 16 and 32 rows, the decode
+  kernel with 4, 5 and 8 rows (one or two queries per group, also of one or
+  two heads), the vector kernel with 1, 2, 4 or 8 rows;
 - n_q = 1 equals kvq_decode_attention bit for bit; results are bitwise
   reproducible.
 - value scales of ~1e-5 (the weight shift from the head's value-scale
@@ -74,8 +75,9 @@ CASES = [
     (W("k2v2_gq2_matrix", 1, 16, 8, 300, 2, 2), 6),                  # two heads: 2-query groups
     (W("k1v1_gq1_rows32", 1, 8, 8, 600, 1, 1), 32),                  # 32 queries of one head per group
     (W("k2v1_gq2_odd", 1, 16, 8, 400, 2, 1), 7),                     # two heads, odd n_q: one query per group
-    (W("k1v1_gq1_g64_vector", 1, 8, 8, 500, 1, 1, gk=64), 8),       # vector kernel, 8 queries per group
-    (W("k2v2_gq2_g64_vector", 1, 16, 8, 300, 2, 2, gk=64), 6),      # vector kernel, 2 queries per group
+    (W("k1v1_gq1_g64_matrix", 1, 8, 8, 500, 1, 1, gk=64), 8),       # matrix kernel, 64-token key groups
+    (W("k1v4_gq1_g64_vector", 1, 8, 8, 500, 1, 4, gk=64), 8),       # vector kernel, 8 queries per group
+    (W("k2v4_gq2_g64_vector", 1, 16, 8, 300, 2, 4, gk=64), 6),      # vector kernel, 2 queries per group
     (W("k1v4_gq4_vector", 1, 32, 8, 800, 1, 4), 9),                  # vector kernel, 4-row groups
     (W("ragged_mixed_g64", 3, 32, 8, (900, 64, 300), (1, 2, 4), (1, 2, 4), gk=64), 33),
     (W("whole_sequence", 1, 32, 8, 48, 1, 1), 48),                   # n_q = L

@@ -45,7 +45,8 @@ CASES = [
     (W("k8v8_gq4_g64", 2, 32, 8, (700, 1111), 8, 8, gk=64), 256, [333, 333, 333, 333]),
     (W("k4v4_gq8", 2, 64, 8, (640, 800), 4, 4), 64, [80, 720]),
     (W("k1v4_gq4_vector", 2, 32, 8, (950, 260), 1, 4), 64, [31, 500, 500]),
-    (W("k2v2_gq2_vector", 2, 16, 8, (700, 333), 2, 2, R=40), 128, [1, 2, 3, 700]),
+    (W("k2v2_gq2_g64", 2, 16, 8, (700, 333), 2, 2, gk=64, R=40), 128, [1, 2, 3, 700]),
+    (W("k2v4_gq2_vector", 2, 16, 8, (700, 333), 2, 4, R=40), 128, [1, 2, 3, 700]),
 ]
 
 

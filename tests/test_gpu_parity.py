@@ -55,10 +55,14 @@ SMALL = [
     W("k4v8_gq4_L1300", 1, 32, 8, 1300, 4, 8),
     W("k8v4_gq5_g64_R40", 2, 40, 8, (900, 1100), 8, 4, gk=64, R=40),
     W("gq8_k4v8_gv64", 1, 64, 8, 700, 4, 8, gv=64),
-    # one or two query heads per kv head on the matrix cores (32-token key groups)
+    # one or two query heads per kv head on the matrix cores (key groups of
+    # 32, 64 and 128 tokens)
     W("gq1_k2v1_L700", 1, 8, 8, 700, 2, 1),
     W("gq2_k1v2_R40_t3", 2, 16, 8, (900, 333), 1, 2, R=40, dist="student_t3"),
     W("gq1_k4v8_L600", 1, 8, 8, 600, 4, 8),
+    W("gq1_k1v1_g64_L1100", 1, 8, 8, 1100, 1, 1, gk=64),
+    W("gq2_k2v2_g128_R40", 2, 16, 8, (1500, 700), 2, 2, gk=128, R=40),
+    W("gq2_k8v4_g64_L900", 1, 16, 8, 900, 8, 4, gk=64),
 ]
 
 
