@@ -470,7 +470,15 @@ decode_mfma_kernel(DecodeArgs a) {
   // 0..3) with distinct column groups share accumulator e (the other
   // columns of their B operand are zero).  Tile pair (2j, 2j + 1) takes
   // column group tile_col(j); lane column xc owns that pair iff they match.
-  f4_t acc[NQ][2];
+  // With two head quads (five or eight heads, two waves per SIMD) the
+  // registers hold one accumulator per tile instead: every column of a
+  // tile's product is kept, the columns of other value groups are dropped
+  // after the loop, and the B operand needs no per-tile zeroing (32 fewer
+  // selects per block).  Not with 8-bit codes, whose blocks leave too few
+  // registers (250-256 with eight accumulators, and slower).
+  constexpr bool kWide = NQ == 2 && BK + BV <= 8;
+  constexpr int NA = kWide ? 8 : 2;
+  f4_t acc[NQ][NA];
 #pragma unroll
   for (int hh = 0; hh < HPL; ++hh) {
     m[hh] = -__builtin_inff();
@@ -482,7 +490,7 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
     for (int t = 0; t < NZ; ++t) zacc[q][t] = 0.f;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) acc[q][e] = (f4_t){0.f, 0.f, 0.f, 0.f};
+    for (int e = 0; e < NA; ++e) acc[q][e] = (f4_t){0.f, 0.f, 0.f, 0.f};
   }
   // Column group of tile pair j: value group g = j * ng / 4 of channels
   // 32j .. 32j + 31 sits in column groups x with x % ng = g; the pairs
@@ -602,7 +610,7 @@ decode_mfma_kernel(DecodeArgs a) {
           av = (H & 1) ? a1 : a0;
         }
 #pragma unroll
-        for (int e = 0; e < 2; ++e) acc[q][e] *= av;
+        for (int e = 0; e < NA; ++e) acc[q][e] *= av;
 #pragma unroll
         for (int t = 0; t < NZ; ++t) zacc[q][t] *= av;
       }
@@ -646,16 +654,18 @@ decode_mfma_kernel(DecodeArgs a) {
         float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
         keep_f32(f0, f1);
         const uint32_t hw = h2u((h2_t){(_Float16)f0, (_Float16)f1});
-        bhi[t] = solo && hc != 0 ? 0u : hw;
+        bhi[t] = !kWide && solo && hc != 0 ? 0u : hw;
         const h2_t z2 = u2h(cur.zv[t]);
         float& za = zacc[q][kPairW ? t : 0];
         za = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, za));
       }
       u4_t bm[4];
+      if constexpr (!kWide) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) bm[j][t] = own[j] ? bhi[t] : 0u;
+          for (int t = 0; t < 4; ++t) bm[j][t] = own[j] ? bhi[t] : 0u;
+      }
 #pragma unroll
       for (int mb = 0; mb < 8; ++mb) {
         h8_t av;
@@ -669,7 +679,10 @@ decode_mfma_kernel(DecodeArgs a) {
         } else {
           av = whole8<BV>(&cur.vx[(BV / 4) * mb]);
         }
-        acc[q][mb & 1] = mfma(av, __builtin_bit_cast(h8_t, bm[mb >> 1]), acc[q][mb & 1]);
+        if constexpr (kWide)
+          acc[q][mb] = mfma(av, __builtin_bit_cast(h8_t, bhi), acc[q][mb]);
+        else
+          acc[q][mb & 1] = mfma(av, __builtin_bit_cast(h8_t, bm[mb >> 1]), acc[q][mb & 1]);
       }
     }
   };
@@ -743,7 +756,11 @@ decode_mfma_kernel(DecodeArgs a) {
     const int ej = ng == 2 ? 2 * (exc & 1) + (exc >> 1) : exc;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      const f4_t v = acc[q][e];
+      f4_t v = acc[q][e];
+      if constexpr (kWide) {  // the tile 2*ej + e (a select chain keeps acc in registers)
+#pragma unroll
+        for (int j = 1; j < 4; ++j) v = ej == j ? acc[q][2 * j + e] : v;
+      }
       if (solo ? ehc == 0 : H < GQ) {
         const int mb = 2 * ej + e;
 #pragma unroll
