@@ -55,6 +55,11 @@ SMALL = [
     W("k4v8_gq4_L1300", 1, 32, 8, 1300, 4, 8),
     W("k8v4_gq5_g64_R40", 2, 40, 8, (900, 1100), 8, 4, gk=64, R=40),
     W("gq8_k4v8_gv64", 1, 64, 8, 700, 4, 8, gv=64),
+    # five and eight heads at 1-4 bits (one value accumulator per tile) with
+    # value groups of 64 and 128 channels
+    W("gq5_k1v1_gv64_R40", 2, 40, 8, (1100, 600), 1, 1, gv=64, R=40),
+    W("gq8_k2v2_gv64", 1, 64, 8, 900, 2, 2, gv=64),
+    W("gq8_k4v4_gv128_g64", 1, 64, 8, 800, 4, 4, gk=64, gv=128),
     # one or two query heads per kv head on the matrix cores (key groups of
     # 32, 64 and 128 tokens)
     W("gq1_k2v1_L700", 1, 8, 8, 700, 2, 1),
