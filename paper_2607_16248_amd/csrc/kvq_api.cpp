@@ -175,13 +175,14 @@ int log2_exact(int v) {
 }
 
 // Split length of one launch's sequences (one bit class): the launch fills
-// one round of the resident workgroups of its kernel, or half a round (two
-// waves per SIMD) for the kernels that run four.  For those, longer splits
-// with fewer waves measured faster: every wave pays a prologue (query,
-// zero-point table, first loads) and an epilogue, all waves' first loads
-// queue behind each other, and the merge reads half the records.  Kernels
-// of two or three waves per SIMD lose their latency hiding at half a round.
-// Classes launch one after another, so each gets the whole device.
+// two workgroups per compute unit (two waves per SIMD), a full round of
+// the kernels that fit two and part of one for those that fit three or
+// four.  Longer splits with fewer waves measured as fast or faster there:
+// every wave pays a prologue (query, zero-point table, first loads) and an
+// epilogue, all waves' first loads queue behind each other, and the merge
+// reads fewer records.  Fewer than two per unit (one wave per SIMD on some
+// units) measured 15-36% slower.  Classes launch one after another, so each
+// gets the whole device.
 int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int nrg, int occ_rows) {
   const int gk = c->d.key_group;
   if (c->split_tokens > 0) return c->split_tokens;
@@ -196,7 +197,7 @@ int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int n
   // The fp16-tail workgroups (one per sequence and kv head with tail tokens)
   // share the same round of resident workgroups: a workgroup that has to
   // wait for a free slot would add a whole split's time to the launch.
-  const int64_t round = target_workgroups(occ) / (occ >= 4 ? 2 : 1);
+  const int64_t round = target_workgroups(std::min(occ, 2));
   const int64_t target = std::max<int64_t>(round - tails, round / 2);
   int64_t st = (total + target - 1) / target;
   if (nrg > 1 && !seqs.empty()) {
