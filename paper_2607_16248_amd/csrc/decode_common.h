@@ -207,8 +207,8 @@ __device__ __forceinline__ int group_limit(const DecodeArgs& a, const DecodeSeq&
   return S.L - a.nqry + 1 + rg * a.qpr;
 }
 
-// (g0: the first row of the group the GQ rows start at; the 16-row chunk
-// kernel takes its fp16 tail in two halves of 8 rows)
+// (g0: the first row of the group the GQ rows start at; the chunk kernel
+// takes its fp16 tail in parts of 8 rows)
 template <int GQ>
 __device__ __forceinline__ void row_limits(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int (&lim)[GQ],
                                            int g0 = 0) {
