@@ -111,14 +111,15 @@ struct BlockData {
   uint32_t kx[2][BK];  // key codes of tokens 16*mb + (lane & 15)
   uint32_t vx[2 * BV]; // value codes of this lane
   u4_t sv, zv;         // value scales / zeros of this lane's 8 tokens and group, element order
+  u4_t sv3, zv3;       // five heads: the same for value group 3 (loaded only there)
 };
 
 // Per-lane byte offsets of one block's loads (the per-block parts are scalar).
 struct LaneOffsets {
-  uint32_t km, kc, vc, vs, vz;
+  uint32_t km, kc, vc, vs, vz, vs3, vz3;
 };
 
-template <int BK, int BV>
+template <int BK, int BV, bool G3>
 __device__ __forceinline__ void load_block(__amdgpu_buffer_rsrc_t r, const LaneOffsets& lo, uint32_t km,
                                            uint32_t kc, uint32_t vc, uint32_t vm, BlockData<BK, BV>& o) {
   o.s = ld32(r, lo.km, km);
@@ -151,6 +152,10 @@ __device__ __forceinline__ void load_block(__amdgpu_buffer_rsrc_t r, const LaneO
   }
   o.sv = ld128(r, lo.vs, vm);
   o.zv = ld128(r, lo.vz, vm);
+  if constexpr (G3) {
+    o.sv3 = ld128(r, lo.vs3, vm);
+    o.zv3 = ld128(r, lo.vz3, vm);
+  }
 }
 
 // The value of quad member K, broadcast to the whole quad (quad_perm
@@ -240,7 +245,15 @@ decode_mfma_kernel(DecodeArgs a) {
   // tokens of K-group row.  Score A rows: row col = head hs, half part.
   const int col = lane & 15, row = lane >> 4;     // MFMA column, lane row
   const int hc = col >> 2, xc = col & 3, part = col & 1, hs = col / RS;
-  const int ng = kHeadDim / a.gv, gsel = xc & (ng - 1);
+  const int ng = kHeadDim / a.gv;
+  // Five heads (with one accumulator per tile): the value columns of one B
+  // operand are (head h1, group g1) = (col % 5, col / 5) for the groups 0 ..
+  // G1 - 1, G1 = min(ng, 3) (15 columns at most; the rest repeat a column),
+  // and with four groups a second operand holds (col, group 3) for col < 5.
+  // 8 value MFMAs per block instead of two head quads' 16.
+  constexpr bool kFive = GQ == 5 && NH / 4 == 2 && BK + BV <= 8;
+  const int g1 = min(col / 5, min(ng, 3) - 1), h1 = col % 5;
+  const int gsel = kFive ? g1 : xc & (ng - 1);
   // row g of the row group reads q row qbase + row_off[g] (row_off[0] = 0)
   const uint16_t* qbase = CAUSAL ? a.q + q_index<GQ, CAUSAL>(a, S, wk.h, wk.rg, 0) * kHeadDim
                                  : a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * GQ) * kHeadDim;
@@ -278,6 +291,8 @@ decode_mfma_kernel(DecodeArgs a) {
   lo.vc = lane * 8 * BV;
   lo.vs = (gsel * 32 + 8 * row) * 2;
   lo.vz = lo.vs + ng * 64;
+  lo.vs3 = (3 * 32 + 8 * row) * 2;
+  lo.vz3 = lo.vs3 + ng * 64;
 
   // This wave's 32-token blocks: key groups j0 + ws + kWaves*n, each of
   // BPG blocks; block i is key group j0 + kWaves*(i / BPG), part i % BPG.
@@ -299,7 +314,7 @@ decode_mfma_kernel(DecodeArgs a) {
     int tok;
     const __amdgpu_buffer_rsrc_t r = seg_of(j * a.gk + (i % BPG) * 32, tok);
     const int jg = paged ? tok >> a.pm.gk_shift : j;  // key group within the segment
-    load_block<BK, BV>(r, lo, a.km + (uint32_t)jg * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
+    load_block<BK, BV, kFive>(r, lo, a.km + (uint32_t)jg * (2 * kHeadDim * 2), a.kc + (uint32_t)tok * 16 * BK,
                        a.vc + (uint32_t)(tok / 32) * 512 * BV, a.vm + (uint32_t)(tok / 32) * vstride, o);
   };
   // Key zero-points of the wave's key groups k0 .. k0 + 15 as the A operand
@@ -600,8 +615,11 @@ decode_mfma_kernel(DecodeArgs a) {
       // the same factors in the value layout: head H = 4q + hc sits in the
       // score lanes of row H / HPL, as their element H % HPL
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int H = (GQ == 5 && q == 1) ? 4 : 4 * q + hc;  // five heads: quad 1 is head 4 alone
+      for (int q = 0; q < (kFive ? 1 : NQ); ++q) {
+        // five heads: both value operands of a lane hold its column's head
+        // h1 (see kFive), one accumulator per tile; else quad 1 is head 4
+        // alone
+        const int H = kFive ? h1 : (GQ == 5 && q == 1) ? 4 : 4 * q + hc;
         float av;
         if constexpr (HPL == 1) {
           av = __shfl(alpha[0], 16 * H);
@@ -612,7 +630,10 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
         for (int e = 0; e < NA; ++e) acc[q][e] *= av;
 #pragma unroll
-        for (int t = 0; t < NZ; ++t) zacc[q][t] *= av;
+        for (int t = 0; t < NZ; ++t) {
+          zacc[q][t] *= av;
+          if constexpr (kFive) zacc[1][t] *= av;
+        }
       }
     }
     // to the value layout: lane (col, row) needs tokens 4*row + 0..3 and
@@ -635,8 +656,55 @@ decode_mfma_kernel(DecodeArgs a) {
       pl[(HPL * row + hh) * kPRow + 16 + col] = e[hh][1];
     }
     wave_lds_sync();
+    if constexpr (kFive) {
+      // Five heads: lane column col carries head h1 = col % 5 in both value
+      // operands, group g1 in the first and group 3 in the second (four
+      // groups); tiles of group 3 take the second, all others the first.
+      const f4_t pa = *reinterpret_cast<const f4_t*>(&pl[h1 * kPRow + 4 * row]);
+      const f4_t pb = *reinterpret_cast<const f4_t*>(&pl[h1 * kPRow + 16 + 4 * row]);
+      const float p[8] = {pa[0], pa[1], pa[2], pa[3], pb[0], pb[1], pb[2], pb[3]};
+      u4_t b1, b3;
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
+      for (int t = 0; t < 4; ++t) {
+        const h2_t s2 = u2h(cur.sv[t]);
+        float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
+        keep_f32(f0, f1);
+        b1[t] = h2u((h2_t){(_Float16)f0, (_Float16)f1});
+        const h2_t z2 = u2h(cur.zv[t]);
+        float& za = zacc[0][kPairW ? t : 0];
+        za = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, za));
+      }
+      b3 = b1;
+      if (ng == 4) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const h2_t s2 = u2h(cur.sv3[t]);
+          float f0 = fmaf(p[2 * t], (float)s2.x, 0.f), f1 = fmaf(p[2 * t + 1], (float)s2.y, 0.f);
+          keep_f32(f0, f1);
+          b3[t] = h2u((h2_t){(_Float16)f0, (_Float16)f1});
+          const h2_t z2 = u2h(cur.zv3[t]);
+          float& za = zacc[1][kPairW ? t : 0];
+          za = fmaf(p[2 * t], (float)z2.x, fmaf(p[2 * t + 1], (float)z2.y, za));
+        }
+      }
+#pragma unroll
+      for (int mb = 0; mb < 8; ++mb) {
+        h8_t av;
+        if constexpr (BV == 1) {
+          av = unpack_bits(cur.vx[mb >> 2], mb & 3);
+        } else if constexpr (BV == 2) {
+          const uint32_t x = cur.vx[mb >> 1] >> (16 * (mb & 1));
+          const uint2 t0 = *reinterpret_cast<const uint2*>(&vtab[(x & 0xFFu) * 2]);
+          const uint2 t1 = *reinterpret_cast<const uint2*>(&vtab[((x >> 8) & 0xFFu) * 2]);
+          av = __builtin_bit_cast(h8_t, (u4_t){t0.x, t0.y, t1.x, t1.y});
+        } else {
+          av = whole8<BV>(&cur.vx[(BV / 4) * mb]);
+        }
+        acc[0][mb] = mfma(av, __builtin_bit_cast(h8_t, mb >= 6 ? b3 : b1), acc[0][mb]);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < (kFive ? 0 : NQ); ++q) {
       // Five heads: the second quad carries head 4 alone (columns 0-3, the
       // rest zero).
       const bool solo = GQ == 5 && q == 1;
@@ -743,8 +811,34 @@ decode_mfma_kernel(DecodeArgs a) {
   // 1-bit, 4- and 8-bit value codes enter the products as code * 2^CodeUnit
   // (2-bit table halves are the codes themselves)
   const float kAccScale = BV == 2 ? 1.f : ldexpf(1.f, -CodeUnit<BV>::value);
+  if constexpr (kFive) {
+    // tile mb (value group g = (mb / 2) * ng / 4): the first operand's lanes
+    // with column 5g .. 5g + 4 (g < min(ng, 3)), or the second's with column
+    // 0 .. 4 (g = 3); head = column % 5
+    float zs[2];
 #pragma unroll
-  for (int q = 0; q < NQ; ++q) {
+    for (int q = 0; q < 2; ++q) {
+      zs[q] = zacc[q][0];
+#pragma unroll
+      for (int t = 1; t < NZ; ++t) zs[q] = fmaf(zacc[q][t], (float)(1 << t), zs[q]);
+      zs[q] += __shfl_xor(zs[q], 16);
+      zs[q] += __shfl_xor(zs[q], 32);
+    }
+    const int H = ecol % 5;
+#pragma unroll
+    for (int mb = 0; mb < 8; ++mb) {
+      const int g = (mb >> 1) * ng / 4;
+      const bool second = ng == 4 && g == 3;
+      const bool mine = second ? ecol < 5 : (ecol < 5 * min(ng, 3) && ecol / 5 == g);
+      if (mine) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          red.acc[wv][H * kHeadDim + 16 * mb + 4 * erow + i] = acc[0][mb][i] * kAccScale + zs[second ? 1 : 0];
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < (kFive ? 0 : NQ); ++q) {
     float zs = zacc[q][0];
 #pragma unroll
     for (int t = 1; t < NZ; ++t) zs = fmaf(zacc[q][t], (float)(1 << t), zs);
