@@ -29,8 +29,11 @@
 //     through LDS.  A tile of 16 channels keeps only the columns of its
 //     value group (the rest of its B operand is zero), so tiles of
 //     different groups share one accumulator: two accumulators hold the
-//     128 channels of 4 heads.  (Five heads: a second quad carries head 4
-//     alone, in its columns 0-3.)
+//     128 channels of 4 heads.  Eight heads take two such head quads; five
+//     heads take columns (head, group) = (col % 5, col / 5) for groups 0-2
+//     and a second operand for group 3 (at 8 bits: a second quad with head
+//     4 alone).  With two operands per block the registers hold one
+//     accumulator per tile instead of sharing them.
 //
 // Packed key codes become operands with a shift or two and one AND per
 // element pair: a set bit at mantissa position w of a half is the exact fp16
