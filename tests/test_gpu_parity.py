@@ -58,6 +58,7 @@ SMALL = [
     # five and eight heads at 1-4 bits (one value accumulator per tile) with
     # value groups of 64 and 128 channels
     W("gq5_k1v1_gv64_R40", 2, 40, 8, (1100, 600), 1, 1, gv=64, R=40),
+    W("gq5_k2v2_gv128_g128", 1, 40, 8, 1300, 2, 2, gk=128, gv=128),
     W("gq8_k2v2_gv64", 1, 64, 8, 900, 2, 2, gv=64),
     W("gq8_k4v4_gv128_g64", 1, 64, 8, 800, 4, 4, gk=64, gv=128),
     # one or two query heads per kv head on the matrix cores (key groups of
