@@ -91,7 +91,7 @@ def read_traffic(name: str):
 
 
 def host_info():
-    """Cores this process may run on and the CPU model (the machine's host, not the build container)."""
+    """Cores this process may run on and the CPU model of the host it runs on."""
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     model = "unknown"
     try:
