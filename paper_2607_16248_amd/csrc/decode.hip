@@ -167,15 +167,50 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
 
 // One workgroup per (sequence, query head, 32-channel slice): thread
 // (part, c) folds the records of splits part, part + 8, ... into a running
-// (max, denominator, channel c numerator), loading kMergeUnroll records at a
-// time so that one memory round trip covers up to 136 splits; the eight
-// parts then meet in LDS.  Four slices per head spread a head's records over
-// four compute units.
+// (max, denominator, channel c numerator), loading U records at a time, U the
+// smallest of 4, 8 and 17 for which one memory round trip covers all splits
+// (up to 32, 64 or 136; loads past the last split would re-read it); the
+// eight parts then meet in LDS.  Four slices per head spread a head's records
+// over four compute units.
 constexpr int kMergeParts = 8;
 constexpr int kMergeSlice = 32;
 constexpr int kMergeSlices = kHeadDim / kMergeSlice;
 constexpr int kMergeThreads = kMergeParts * kMergeSlice;
-constexpr int kMergeUnroll = 17;
+
+template <int U>
+__device__ __forceinline__ void merge_fold(const float* base, size_t step, int n, int part, int c, float& M,
+                                           float& D, float& A) {
+  for (int i0 = part; i0 < n; i0 += kMergeParts * U) {
+    float mv[U], lv[U], av[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = i0 + kMergeParts * u;
+      const float* r = base + (size_t)min(i, n - 1) * step;
+      mv[u] = r[0];
+      lv[u] = r[1];
+      av[u] = r[4 + c];
+    }
+    float mx = M;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (i0 + kMergeParts * u < n) mx = fmaxf(mx, mv[u]);
+    // M = -inf on the first batch: f = 0.  A split that saw no token of a
+    // chunk query's row has m = -inf (l = 0, acc = 0); while every record so
+    // far is such a split, mx = -inf and nothing is added.
+    const bool none = mx == -__builtin_inff();
+    const float f = none ? 1.f : __builtin_amdgcn_exp2f(M - mx);
+    D *= f;
+    A *= f;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (i0 + kMergeParts * u < n) {
+        const float w = none ? 0.f : __builtin_amdgcn_exp2f(mv[u] - mx);
+        D = fmaf(w, lv[u], D);
+        A = fmaf(w, av[u], A);
+      }
+    M = mx;
+  }
+}
 
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
   __shared__ float sm[kMergeParts], sl[kMergeParts], sa[kMergeParts][kMergeSlice];
@@ -193,36 +228,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
   const float* base = a.ws + ((size_t)S.ws_base * a.hq + hq) * kRecFloats;
   const size_t step = (size_t)a.hq * kRecFloats;
   float M = -__builtin_inff(), D = 0.f, A = 0.f;
-  for (int i0 = part; i0 < n; i0 += kMergeParts * kMergeUnroll) {
-    float mv[kMergeUnroll], lv[kMergeUnroll], av[kMergeUnroll];
-#pragma unroll
-    for (int u = 0; u < kMergeUnroll; ++u) {
-      const int i = i0 + kMergeParts * u;
-      const float* r = base + (size_t)min(i, n - 1) * step;
-      mv[u] = r[0];
-      lv[u] = r[1];
-      av[u] = r[4 + c];
-    }
-    float mx = M;
-#pragma unroll
-    for (int u = 0; u < kMergeUnroll; ++u)
-      if (i0 + kMergeParts * u < n) mx = fmaxf(mx, mv[u]);
-    // M = -inf on the first batch: f = 0.  A split that saw no token of a
-    // chunk query's row has m = -inf (l = 0, acc = 0); while every record so
-    // far is such a split, mx = -inf and nothing is added.
-    const bool none = mx == -__builtin_inff();
-    const float f = none ? 1.f : __builtin_amdgcn_exp2f(M - mx);
-    D *= f;
-    A *= f;
-#pragma unroll
-    for (int u = 0; u < kMergeUnroll; ++u)
-      if (i0 + kMergeParts * u < n) {
-        const float w = none ? 0.f : __builtin_amdgcn_exp2f(mv[u] - mx);
-        D = fmaf(w, lv[u], D);
-        A = fmaf(w, av[u], A);
-      }
-    M = mx;
-  }
+  if (n <= kMergeParts * 4) merge_fold<4>(base, step, n, part, c, M, D, A);
+  else if (n <= kMergeParts * 8) merge_fold<8>(base, step, n, part, c, M, D, A);
+  else merge_fold<17>(base, step, n, part, c, M, D, A);
   if (cs == 0) {
     sm[part] = M;
     sl[part] = D;

@@ -140,7 +140,9 @@ def test_split_independence_and_determinism():
     c.append_all()
     ref = c.oracle_out(0)
     outs = {}
-    for st in (128, 256, 1024, 4096, 0):
+    # 129, 65, 33, 17, 5 and 2 records per head: the merge loads 17, 17, 8,
+    # 4, 4 and 4 records per round trip
+    for st in (32, 64, 128, 256, 1024, 4096, 0):
         kvq_set = __import__("paper_2607_16248_amd").kvq_set_split_tokens
         kvq_set(c.cache.handle, st)
         a = c.decode()
