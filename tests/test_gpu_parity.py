@@ -154,6 +154,24 @@ def test_split_independence_and_determinism():
         assert row_rel_err(a[0], outs[128][0].astype(np.float64)).max() <= ATTN_TOL
 
 
+@pytest.mark.parametrize("L,st,n", [(4096, 128, 32), (4096, 64, 64), (4352, 32, 136), (4384, 32, 137)])
+def test_merge_at_its_load_counts(L, st, n):
+    # exactly 32, 64 and 136 records per head (the largest counts one round
+    # trip of 4, 8 and 17 loads per thread covers) and 137 (two rounds of 17)
+    w = W(f"merge_n{n}", 1, 32, 8, L, 1, 1)
+    c = Case(w)
+    c.append_all()
+    kvq_set = __import__("paper_2607_16248_amd").kvq_set_split_tokens
+    kvq_set(c.cache.handle, st)
+    assert -(-L // st) == n
+    a = c.decode()
+    b = c.decode()
+    assert (a.view(np.uint32) == b.view(np.uint32)).all()
+    err = row_rel_err(a[0], c.oracle_out(0)).max()
+    log(f"[parity] {n} records per head: max row-relative error {err:.3e}")
+    assert err <= ATTN_TOL
+
+
 @pytest.mark.parametrize("gk,bk,bv", [(32, 1, 1), (64, 2, 1), (128, 1, 2), (32, 8, 8), (64, 4, 4)])
 def test_long_splits(gk, bk, bv):
     # One split per head: every wave of the matrix kernel takes more than
