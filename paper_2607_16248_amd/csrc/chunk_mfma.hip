@@ -231,7 +231,7 @@ chunk_mfma_kernel(DecodeArgs a) {
   uint32_t qw[R / kWaves];
 #pragma unroll
   for (int i = 0; i < R / kWaves; ++i)
-    qw[i] = reinterpret_cast<const uint32_t*>(qbase + (size_t)a.row_off[wv + kWaves * i] * kHeadDim)[lane];
+    qw[i] = reinterpret_cast<const uint32_t*>(qbase + (size_t)row_q_offset(a, wk.rg, wv + kWaves * i) * kHeadDim)[lane];
   constexpr int kTabLoads = BV == 2 ? ValueTable2::kWords / 4 : 0;
   u4_t tabw = {0u, 0u, 0u, 0u};
   if constexpr (kTabLoads > 0) {

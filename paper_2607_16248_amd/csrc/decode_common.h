@@ -182,13 +182,29 @@ __device__ __forceinline__ Work find_work(const DecodeArgs& a) {
   return w;
 }
 
+// Chunk queries: when qpr does not divide nqry, the last row group holds
+// fewer queries; its rows past the last query repeat the last query (they
+// read its q row and see its tokens, so every access stays in bounds) and
+// write no record.
+__device__ __forceinline__ bool row_padded(const DecodeArgs& a, int rg, int g) {
+  return rg * a.qpr + a.row_x[g] >= a.nqry;
+}
+// the query row g computes: rg * qpr + row_x[g], or the last query
+__device__ __forceinline__ int row_query(const DecodeArgs& a, int rg, int g) {
+  return min(rg * a.qpr + a.row_x[g], a.nqry - 1);
+}
+// offset of row g's q row from that of the row group's row 0 (a valid query)
+__device__ __forceinline__ int row_q_offset(const DecodeArgs& a, int rg, int g) {
+  return a.row_off[g] - (rg * a.qpr + a.row_x[g] - row_query(a, rg, g)) * a.hq;
+}
+
 // Row g of the workgroup's row group: its index in q / out
 // ([batch][nqry][Hq]), its record row within a split (query * Hq + head),
 // and the end of the tokens it sees.
 template <int GQ, bool CHUNK>
 __device__ __forceinline__ size_t q_index(const DecodeArgs& a, const DecodeSeq& S, int h, int rg, int g) {
   if constexpr (!CHUNK) return (size_t)S.seq * a.hq + (size_t)h * GQ + g;
-  return ((size_t)S.seq * a.nqry + rg * a.qpr) * a.hq + h * a.gqh + a.row_off[g];
+  return ((size_t)S.seq * a.nqry + rg * a.qpr) * a.hq + h * a.gqh + row_q_offset(a, rg, g);
 }
 
 template <int GQ, bool CHUNK>
@@ -198,7 +214,7 @@ __device__ __forceinline__ int rec_row(const DecodeArgs& a, int h, int rg, int g
 }
 
 __device__ __forceinline__ int row_limit(const DecodeArgs& a, const DecodeSeq& S, int rg, int g) {
-  return S.L - a.nqry + 1 + rg * a.qpr + a.row_x[g];
+  return S.L - a.nqry + 1 + row_query(a, rg, g);
 }
 
 // The smallest limit of the row group: every token below it is visible to
@@ -255,6 +271,7 @@ __device__ __forceinline__ void write_record(const DecodeArgs& a, const DecodeSe
                                              const Reduce<GQ>& r, int g0 = 0) {
   for (int idx = threadIdx.x; idx < GQ * kHeadDim; idx += blockDim.x) {
     const int g = idx / kHeadDim, c = idx % kHeadDim;
+    if (CHUNK && row_padded(a, rg, g0 + g)) continue;  // a repeat of the last query
     float M = -__builtin_inff();
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) M = fmaxf(M, r.m[w][g]);

@@ -257,7 +257,7 @@ decode_mfma_kernel(DecodeArgs a) {
   constexpr bool kFive = GQ == 5 && NH / 4 == 2 && BK + BV <= 8;
   const int g1 = min(col / 5, min(ng, 3) - 1), h1 = col % 5;
   const int gsel = kFive ? g1 : xc & (ng - 1);
-  // row g of the row group reads q row qbase + row_off[g] (row_off[0] = 0)
+  // row g of the row group reads q row qbase + row_q_offset(g) (0 for row 0)
   const uint16_t* qbase = CAUSAL ? a.q + q_index<GQ, CAUSAL>(a, S, wk.h, wk.rg, 0) * kHeadDim
                                  : a.q + ((size_t)S.seq * a.hq + (size_t)wk.h * GQ) * kHeadDim;
   // Packed data: the (sequence, head) region, or in a paged cache this kv
@@ -349,7 +349,7 @@ decode_mfma_kernel(DecodeArgs a) {
 #pragma unroll
   for (int i = 0; i < kOwn; ++i) {
     const int g = wv + kWaves * i;
-    qw[i] = g < GQ ? reinterpret_cast<const uint32_t*>(qbase + (size_t)(CAUSAL ? a.row_off[g] : g) * kHeadDim)[lane]
+    qw[i] = g < GQ ? reinterpret_cast<const uint32_t*>(qbase + (size_t)(CAUSAL ? row_q_offset(a, wk.rg, g) : g) * kHeadDim)[lane]
                    : 0u;
   }
   constexpr int kTabLoads = BV == 2 ? ValueTable2::kWords / 4 : 0;

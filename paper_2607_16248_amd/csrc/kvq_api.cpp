@@ -505,34 +505,56 @@ struct Rows {
 };
 
 // Single-token decode: one row group of the kv head's query heads.  Chunk
-// queries: the largest row group a kernel has (matrix: 32 rows in the chunk
-// kernel for 1- and 2-bit classes, 16 for those and 4-bit classes, with
-// value groups of 32 channels; 4, 5, 8 in the decode kernel; vector: also
-// 1, 2) made of whole queries, with a whole number of groups.
+// queries on the vector kernel: the largest of its row groups (8, 5, 4, 2,
+// 1 rows) made of whole queries, with a whole number of groups.  On the
+// matrix cores (32 rows in the chunk kernel for 1- and 2-bit classes, 16 for
+// those and 4-bit classes, with value groups of 32 channels; 8, 5 or 4 in
+// the decode kernel), the row group of whole queries with the smallest
+// estimated time: ceil(nqry / qpr) passes over the kv head's cache at a
+// per-pass cost that grows with the rows; the last group may repeat the last
+// query in its spare rows.
+// Relative cost of one pass per row count: µs per row group of 131072-token
+// K1V1 Llama-3.1-8B layers when a chunk launch takes several (4-row 16,
+// 8-row 19, 16-row 27, 32-row 42; a launch's first pass costs ~12 µs more).
+int pass_cost(int rows) { return rows >= 32 ? 42 : rows >= 16 ? 27 : rows >= 8 ? 19 : rows >= 5 ? 17 : 16; }
+
 Rows rows_for(const kvq_cache* c, bool matrix, int nqry, int bk, int bv) {
   const int gqh = c->d.num_q_heads / c->d.num_kv_heads;
   Rows r;
   r.rows = gqh;
   if (nqry <= 1) return r;
-  static const int kMatrixRows[] = {32, 16, 8, 5, 4}, kVectorRows[] = {8, 5, 4, 2, 1};
-  const int* cand = matrix ? kMatrixRows : kVectorRows;
-  const int ncand = 5;
-  const bool rows16 = matrix && c->d.value_group == 32 && bk + bv <= 8;
   r.nqry = nqry;
-  for (int k = 0; k < ncand; ++k) {
-    const int rg = cand[k];
+  if (!matrix) {
+    for (int rg : {8, 5, 4, 2, 1}) {
+      if (rg % gqh == 0 && nqry % (rg / gqh) == 0) {
+        r.qpr = rg / gqh;
+        r.nrg = nqry / r.qpr;
+        r.rows = rg;
+        return r;
+      }
+    }
+    r.qpr = 1;  // not reached: rg = gqh always qualifies
+    r.nrg = nqry;
+    return r;
+  }
+  const bool rows16 = c->d.value_group == 32 && bk + bv <= 8;
+  r.qpr = 1;  // one query per group (rows = gqh) unless a candidate is cheaper
+  r.nrg = nqry;
+  int best = -1;
+  for (int rg : {32, 16, 8, 5, 4}) {
     if (rg >= 16 && !rows16) continue;
     if (rg == 32 && !kvq::chunk_rows32(bk, bv)) continue;
-    if (rg % gqh == 0 && nqry % (rg / gqh) == 0) {
-      r.qpr = rg / gqh;
-      r.nrg = nqry / r.qpr;
+    if (rg % gqh != 0) continue;
+    const int qpr = rg / gqh, nrg = (nqry + qpr - 1) / qpr;
+    const int cost = nrg * pass_cost(rg);
+    if (best < 0 || cost < best) {
+      best = cost;
+      r.qpr = qpr;
+      r.nrg = nrg;
       r.rows = rg;
-      return r;
     }
   }
-  r.qpr = 1;  // not reached: rg = gqh always qualifies
-  r.nrg = nqry;
-  return r;
+  return r;  // 4 rows (1, 2 or 4 heads), 5 or 8 always qualify
 }
 
 struct SplitPlan {

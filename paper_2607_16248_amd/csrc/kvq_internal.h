@@ -139,7 +139,8 @@ struct DecodeSeq {
 // (nqry = 1: single-token decode over the whole cache).  The rows of one kv
 // head h are (query j, head h*gqh + x); a workgroup takes a row group of qpr
 // consecutive queries times the gqh heads (GQ = qpr*gqh rows, the kernel's
-// template size), row group rg of nrg = nqry / qpr.  q and out are
+// template size), row group rg of nrg = ceil(nqry / qpr) (the last one
+// may repeat the last query in its spare rows).  q and out are
 // [batch][nqry][Hq][128]; a split record row is j*Hq + head.
 struct DecodeArgs {
   const uint8_t* arena;

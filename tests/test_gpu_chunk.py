@@ -8,7 +8,9 @@ seeded, byte-identical cache, through the C ABI.
   query sees one token: its value row);
 - every row-group shape: the chunk kernel with 16 and 32 rows, the decode
   kernel with 4, 5 and 8 rows (one or two queries per group, also of one or
-  two heads), the vector kernel with 1, 2, 4 or 8 rows;
+  two heads), the vector kernel with 1, 2, 4 or 8 rows; on the matrix cores
+  a last row group with spare rows (n_q not a multiple of its queries: the
+  spare rows repeat the last query and write nothing);
 - n_q = 1 equals kvq_decode_attention bit for bit; results are bitwise
   reproducible.
 - value scales of ~1e-5 (the weight shift from the head's value-scale
@@ -66,7 +68,7 @@ def _check(c, q, out, heads=None):
 
 CASES = [
     (W("k1v1_gq4_L1000", 1, 32, 8, 1000, 1, 1), 40),                 # masks inside packed blocks; 32-row groups
-    (W("k2v2_gq4_L777_odd", 1, 32, 8, 777, 2, 2), 7),                # odd n_q: 4-row groups
+    (W("k2v2_gq4_L777_odd", 1, 32, 8, 777, 2, 2), 7),                # odd n_q: one 32-row group, a spare query
     (W("k2v2_gq5_R128_t3", 2, 40, 8, (600, 333), 2, 2, R=128, dist="student_t3"), 16),  # masks in the fp16 tail
     (W("k4v4_gq8_g64", 1, 64, 8, 900, 4, 4, gk=64), 5),
     (W("k8v8_gq4", 1, 32, 8, 700, 8, 8), 12),
@@ -74,7 +76,7 @@ CASES = [
     (W("k1v1_gq1_matrix", 1, 8, 8, 500, 1, 1), 8),                   # one head per kv head: 8-query groups
     (W("k2v2_gq2_matrix", 1, 16, 8, 300, 2, 2), 6),                  # two heads: 2-query groups
     (W("k1v1_gq1_rows32", 1, 8, 8, 600, 1, 1), 32),                  # 32 queries of one head per group
-    (W("k2v1_gq2_odd", 1, 16, 8, 400, 2, 1), 7),                     # two heads, odd n_q: one query per group
+    (W("k2v1_gq2_odd", 1, 16, 8, 400, 2, 1), 7),                     # two heads, odd n_q: one 16-row group, a spare query
     (W("k1v1_gq1_g64_matrix", 1, 8, 8, 500, 1, 1, gk=64), 8),       # matrix kernel, 64-token key groups
     (W("k1v4_gq1_g64_vector", 1, 8, 8, 500, 1, 4, gk=64), 8),       # vector kernel, 8 queries per group
     (W("k2v4_gq2_g64_vector", 1, 16, 8, 300, 2, 4, gk=64), 6),      # vector kernel, 2 queries per group
@@ -90,6 +92,11 @@ CASES = [
     (W("k2v2_gq4_rows16", 1, 32, 8, 650, 2, 2), 12),
     (W("k2v1_gq4_rows32_g64", 2, 32, 8, (1000, 517), 2, 1, gk=64), 8),
     (W("k1v2_gq8_rows32", 1, 64, 8, 700, 1, 2), 4),
+    # spare rows in the last row group: 32 rows with three spare queries,
+    # 16 rows of one head with three, 8 rows (decode kernel) with one
+    (W("k1v1_gq4_pad32", 1, 32, 8, 900, 1, 1), 5),
+    (W("k1v1_gq1_pad16", 2, 8, 8, (600, 450), 1, 1), 13),
+    (W("k8v8_gq4_pad8", 1, 32, 8, 700, 8, 8), 3),
 ]
 
 

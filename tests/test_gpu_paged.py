@@ -122,7 +122,7 @@ def test_release_reuses_pages_and_pool_capacity():
     assert row_rel_err(out[1], c.oracle_out(1)).max() <= ATTN_TOL
 
 
-@pytest.mark.parametrize("n_q", [24, 7])   # 8-row groups; 4-row groups (odd n_q)
+@pytest.mark.parametrize("n_q", [24, 7])   # three 32-row groups; one with a spare query (odd n_q)
 def test_chunk_attention_over_pages(n_q):
     from paper_2607_16248_amd import kvq
     w = W("chunk_paged", 2, 32, 8, (1200, 777), 1, 1)
