@@ -514,9 +514,10 @@ struct Rows {
 // per-pass cost that grows with the rows; the last group may repeat the last
 // query in its spare rows.
 // Relative cost of one pass per row count: µs per row group of 131072-token
-// K1V1 Llama-3.1-8B layers when a chunk launch takes several (4-row 16,
-// 8-row 19, 16-row 27, 32-row 42; a launch's first pass costs ~12 µs more).
-int pass_cost(int rows) { return rows >= 32 ? 42 : rows >= 16 ? 27 : rows >= 8 ? 19 : rows >= 5 ? 17 : 16; }
+// K1V1 Llama-3.1-8B layers when a chunk launch takes several (4-row 18,
+// 8-row 21, 16-row 30, 32-row 38; a launch's first pass costs 10-20 µs
+// more).
+int pass_cost(int rows) { return rows >= 32 ? 38 : rows >= 16 ? 30 : rows >= 8 ? 21 : rows >= 5 ? 19 : 18; }
 
 Rows rows_for(const kvq_cache* c, bool matrix, int nqry, int bk, int bv) {
   const int gqh = c->d.num_q_heads / c->d.num_kv_heads;

@@ -74,7 +74,9 @@ CASES = [
     (W("k8v8_gq4", 1, 32, 8, 700, 8, 8), 12),
     (W("k1v2_gq4_g128", 1, 32, 8, 1500, 1, 2, gk=128), 24),
     (W("k1v1_gq1_matrix", 1, 8, 8, 500, 1, 1), 8),                   # one head per kv head: 8-query groups
-    (W("k2v2_gq2_matrix", 1, 16, 8, 300, 2, 2), 6),                  # two heads: 2-query groups
+    (W("k2v2_gq2_matrix", 1, 16, 8, 300, 2, 2), 2),                  # two heads: one 2-query group (4 rows)
+    (W("k2v2_gq2_pad16", 1, 16, 8, 300, 2, 2), 6),                   # two heads: one 16-row group, two spare queries
+    (W("k1v1_gq1_rows5", 1, 8, 8, 500, 1, 1), 5),                    # one head: one 5-query group
     (W("k1v1_gq1_rows32", 1, 8, 8, 600, 1, 1), 32),                  # 32 queries of one head per group
     (W("k2v1_gq2_odd", 1, 16, 8, 400, 2, 1), 7),                     # two heads, odd n_q: one 16-row group, a spare query
     (W("k1v1_gq1_g64_matrix", 1, 8, 8, 500, 1, 1, gk=64), 8),       # matrix kernel, 64-token key groups
@@ -84,12 +86,12 @@ CASES = [
     (W("ragged_mixed_g64", 3, 32, 8, (900, 64, 300), (1, 2, 4), (1, 2, 4), gk=64), 33),
     (W("whole_sequence", 1, 32, 8, 48, 1, 1), 48),                   # n_q = L
     # the chunk kernel: 16-row groups (2 queries x 8 heads at 4 bits, 4 x 4 at
-    # 1 and 2 bits where 8 queries do not divide n_q) and 32-row groups (two
-    # row halves: 8 x 4 over two ragged sequences with 64-token key groups
-    # and 1-bit values, 4 x 8 heads)
+    # 1 and 2 bits for up to 4 queries) and 32-row groups (two row halves:
+    # 8 x 4 over two ragged sequences with 64-token key groups and 1-bit
+    # values, 4 x 8 heads)
     (W("k4v4_gq8_rows16", 1, 64, 8, 900, 4, 4), 6),
     (W("k1v1_gq4_rows16", 1, 32, 8, 700, 1, 1), 4),
-    (W("k2v2_gq4_rows16", 1, 32, 8, 650, 2, 2), 12),
+    (W("k2v2_gq4_rows16", 1, 32, 8, 650, 2, 2), 3),
     (W("k2v1_gq4_rows32_g64", 2, 32, 8, (1000, 517), 2, 1, gk=64), 8),
     (W("k1v2_gq8_rows32", 1, 64, 8, 700, 1, 2), 4),
     # spare rows in the last row group: 32 rows with three spare queries,
