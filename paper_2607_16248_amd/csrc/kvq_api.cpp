@@ -512,7 +512,8 @@ struct Rows {
 // the decode kernel), the row group of whole queries with the smallest
 // estimated time: ceil(nqry / qpr) passes over the kv head's cache at a
 // per-pass cost that grows with the rows; the last group may repeat the last
-// query in its spare rows.
+// query in its spare rows, and a chunk kernel group of five heads leaves the
+// rows past its 3 or 6 queries spare.
 // Relative cost of one pass per row count: µs per row group of 131072-token
 // K1V1 Llama-3.1-8B layers when a chunk launch takes several (4-row 18,
 // 8-row 21, 16-row 30, 32-row 38; a launch's first pass costs 10-20 µs
@@ -545,7 +546,10 @@ Rows rows_for(const kvq_cache* c, bool matrix, int nqry, int bk, int bv) {
   for (int rg : {32, 16, 8, 5, 4}) {
     if (rg >= 16 && !rows16) continue;
     if (rg == 32 && !kvq::chunk_rows32(bk, bv)) continue;
-    if (rg % gqh != 0) continue;
+    // the decode kernel's row layouts hold whole sets of heads; the chunk
+    // kernel's 16 or 32 rows take floor(rows / gqh) queries (five heads: 3
+    // or 6) and leave the remaining rows spare
+    if (rg < 16 && rg % gqh != 0) continue;
     const int qpr = rg / gqh, nrg = (nqry + qpr - 1) / qpr;
     const int cost = nrg * pass_cost(rg);
     if (best < 0 || cost < best) {
@@ -628,8 +632,10 @@ kvq_status run_partials(const kvq_cache* c, const SplitPlan& p, const void* q, v
     a.qscale = qscale;
     const Rows r = rows_for(c, c->matrix[cls.second[0]] != 0, p.nqry, cls.first.first, cls.first.second);
     a.nqry = r.nqry; a.qpr = r.qpr; a.nrg = r.nrg; a.gqh = d.num_q_heads / d.num_kv_heads;
+    // rows past qpr whole queries (a chunk kernel group of five heads) are
+    // spare: row_x = kvq::kSpareRow marks them (a repeat of the last query)
     for (int g = 0; g < 32; ++g) {
-      a.row_x[g] = g / a.gqh;
+      a.row_x[g] = g < r.qpr * a.gqh ? g / a.gqh : kvq::kSpareRow;
       a.row_off[g] = a.row_x[g] * d.num_q_heads + g % a.gqh;
     }
     a.pm = c->pm;

@@ -24,6 +24,9 @@ namespace kvq {
 
 constexpr int kHeadDim = 128;
 constexpr int kMaxSeqPerLaunch = 64;   // sequences described in one kernel-argument block
+// row_x of the rows of a chunk row group past its whole queries: any value
+// at least the largest n_q (1024) makes such a row spare
+constexpr int32_t kSpareRow = 1 << 20;
 constexpr int kRecFloats = 132;        // split record: m, l, 2 pad, acc[128]
 constexpr uint64_t kAlign = 256;
 constexpr uint64_t kHeaderBytes = 256;
@@ -161,7 +164,8 @@ struct DecodeArgs {
   // so that single-token decode reads the same argument lines as before)
   int32_t nqry, qpr, nrg, gqh;
   // row g of a row group is chunk query rg*qpr + row_x[g] and head
-  // h*gqh + (row_off[g] - row_x[g]*Hq): row_off[g] = row_x[g]*Hq + g % gqh
+  // h*gqh + (row_off[g] - row_x[g]*Hq): row_off[g] = row_x[g]*Hq + g % gqh;
+  // rows past the group's qpr*gqh have row_x = kSpareRow (always spare)
   // (host-computed, so the kernels divide nothing)
   int32_t row_off[32], row_x[32];
   PageMap pm;

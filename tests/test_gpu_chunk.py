@@ -69,7 +69,7 @@ def _check(c, q, out, heads=None):
 CASES = [
     (W("k1v1_gq4_L1000", 1, 32, 8, 1000, 1, 1), 40),                 # masks inside packed blocks; 32-row groups
     (W("k2v2_gq4_L777_odd", 1, 32, 8, 777, 2, 2), 7),                # odd n_q: one 32-row group, a spare query
-    (W("k2v2_gq5_R128_t3", 2, 40, 8, (600, 333), 2, 2, R=128, dist="student_t3"), 16),  # masks in the fp16 tail
+    (W("k2v2_gq5_R128_t3", 2, 40, 8, (600, 333), 2, 2, R=128, dist="student_t3"), 16),  # masks in the fp16 tail; five heads, 32 rows
     (W("k4v4_gq8_g64", 1, 64, 8, 900, 4, 4, gk=64), 5),
     (W("k8v8_gq4", 1, 32, 8, 700, 8, 8), 12),
     (W("k1v2_gq4_g128", 1, 32, 8, 1500, 1, 2, gk=128), 24),
@@ -99,6 +99,10 @@ CASES = [
     (W("k1v1_gq4_pad32", 1, 32, 8, 900, 1, 1), 5),
     (W("k1v1_gq1_pad16", 2, 8, 8, (600, 450), 1, 1), 13),
     (W("k8v8_gq4_pad8", 1, 32, 8, 700, 8, 8), 3),
+    # five heads in the chunk kernel: 6 queries in 32 rows (two rows spare),
+    # 3 in 16 (one row spare), each with spare queries in the last group
+    (W("k1v1_gq5_rows32", 1, 40, 8, 800, 1, 1), 16),
+    (W("k4v4_gq5_rows16", 2, 40, 8, (600, 333), 4, 4), 4),
 ]
 
 
