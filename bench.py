@@ -354,7 +354,24 @@ def dgap_leg(workload_idx: int, bits: int, iters: int):
     return out
 
 
-CHUNK_SIZES = (4, 16, 64)
+CHUNK_SIZES = (4, 5, 16, 64)
+
+
+def chunk_row_groups(n_q: int, gq: int):
+    """Rows per group and groups per kv head as the library plans chunk
+    queries on 1- and 2-bit caches with value groups of 32: of 32 or 16 rows
+    (the chunk kernel, floor(rows / gq) queries each) and 8, 5 or 4 (the
+    decode kernel, whole sets of heads), the one with the fewest estimated
+    microseconds, ceil(n_q / queries) passes at 38, 30, 21, 19 or 18."""
+    cost = {32: 38, 16: 30, 8: 21, 5: 19, 4: 18}
+    best = None
+    for r in (32, 16, 8, 5, 4):
+        if (r < 16 and r % gq) or r // gq == 0:
+            continue
+        n = -(-n_q // (r // gq))
+        if best is None or n * cost[r] < best[0]:
+            best = (n * cost[r], r, n)
+    return best[1], best[2]
 
 
 def chunk_leg(handles, w, launch_bytes: int, stream, iters: int):
@@ -368,7 +385,7 @@ def chunk_leg(handles, w, launch_bytes: int, stream, iters: int):
     dev = torch.device("cuda:0")
     layers = len(handles)
     out = {"n_q": list(CHUNK_SIZES), "us_per_layer": [], "query_tokens_per_s_per_layer": [],
-           "cache_gbs_one_pass": [], "useful_tflops": [], "row_groups_per_kv_head": []}
+           "cache_gbs_one_pass": [], "useful_tflops": [], "row_groups_per_kv_head": [], "rows_per_group": []}
     L = min(kvq.kvq_seq_len(handles[0], s) for s in range(w.batch))
     for n_q in CHUNK_SIZES:
         g = torch.Generator(device=dev).manual_seed(n_q)
@@ -388,21 +405,19 @@ def chunk_leg(handles, w, launch_bytes: int, stream, iters: int):
         us = a.elapsed_time(b) * 1e3 / iters
         # QK and PV: 2 * 2 * d flops per (query, head, visible token)
         flops = 4 * w.head_dim * w.num_q_heads * w.batch * sum(L - n_q + 1 + i for i in range(n_q))
-        gq = w.group_q
-        # the row groups the library forms (K1V1, value groups of 32): 32 or
-        # 16 rows when whole queries fill them, else 8 or the query heads of a
-        # kv head
-        rows = next((r for r in (32, 16) if r % gq == 0 and n_q % (r // gq) == 0),
-                    8 if (gq == 4 and n_q % 2 == 0) or gq == 8 else gq)
+        rows, groups = chunk_row_groups(n_q, w.group_q)
         out["us_per_layer"].append(round(us, 3))
         out["query_tokens_per_s_per_layer"].append(round(n_q * w.batch / (us * 1e-6), 1))
         out["cache_gbs_one_pass"].append(round(launch_bytes / (us * 1e-6) / 1e9, 2))
         out["useful_tflops"].append(round(flops / (us * 1e-6) / 1e12, 2))
-        out["row_groups_per_kv_head"].append(n_q * gq // rows)
+        out["row_groups_per_kv_head"].append(groups)
+        out["rows_per_group"].append(rows)
         del q, o, ws
     out["note"] = ("each row group of up to 32 (query, head) rows is one pass over the kv head's cache "
-                   "(the chunk kernel: two row halves of 16 share each unpacked code operand); the useful flops "
-                   "count each visible (query, head, token) once")
+                   "(the chunk kernel: two row halves of 16 share each unpacked code operand); a last group "
+                   "with fewer queries repeats the last one in its spare rows (n_q = 5: one 32-row group, the "
+                   "verification step of 4 drafted tokens); the useful flops count each visible (query, head, "
+                   "token) once")
     # the matrix-core roofline of the contraction (fp16 operands, fp32 accumulation)
     out["roofline"] = {"bound": "mfma", "peak": MFMA_FP16_PEAK_TFLOPS, "unit": "TFLOP/s",
                        "frac": [round(t / MFMA_FP16_PEAK_TFLOPS, 4) for t in out["useful_tflops"]]}
