@@ -24,6 +24,7 @@
 using kvq::HeadLayout;
 
 static_assert(kvq::kScratchBytes == KVQ_NOALLOC_SCRATCH_BYTES, "scratch array size as the header states");
+static_assert(kvq::kSpareRow >= KVQ_MAX_CHUNK, "a spare row lies past every chunk query");
 
 struct kvq_cache {
   kvq_cache_desc d{};

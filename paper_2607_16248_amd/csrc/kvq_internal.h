@@ -25,8 +25,9 @@ namespace kvq {
 constexpr int kHeadDim = 128;
 constexpr int kMaxSeqPerLaunch = 64;   // sequences described in one kernel-argument block
 // row_x of the rows of a chunk row group past its whole queries: any value
-// at least the largest n_q (1024) makes such a row spare
-constexpr int32_t kSpareRow = 1 << 20;
+// at least the largest n_q (KVQ_MAX_CHUNK = 1024) makes such a row spare,
+// and kSpareRow * Hq stays far inside 32 bits
+constexpr int32_t kSpareRow = 1024;
 constexpr int kRecFloats = 132;        // split record: m, l, 2 pad, acc[128]
 constexpr uint64_t kAlign = 256;
 constexpr uint64_t kHeaderBytes = 256;
