@@ -11,6 +11,7 @@
 #include "kvq.h"
 
 extern int g_launches;
+extern int g_row_plans;
 
 static int g_fail = 0;
 #define EXPECT(cond)                                                    \
@@ -107,7 +108,7 @@ static void exercise(const kvq_cache_desc& d) {
     EXPECT(kvq_decode_attention_noalloc(c, q.p, out.as<float>(), nullptr) == KVQ_OK);
     int64_t Lmin = T;
     for (int s = 0; s < B; ++s) Lmin = std::min<int64_t>(Lmin, kvq_seq_len(c, s));
-    for (int nq : {1, 7, 64}) {
+    for (int nq : {1, 2, 3, 5, 7, 13, 33, 64}) {
       if (nq > Lmin) continue;
       const size_t cw = kvq_chunk_workspace_bytes(c, nq);
       Buf cws(cw + 16);
@@ -196,6 +197,6 @@ int main() {
     std::fprintf(stderr, "%d host checks failed\n", g_fail);
     return 1;
   }
-  std::printf("host checks ok (%d launches)\n", g_launches);
+  std::printf("host checks ok (%d launches, %d chunk row plans checked)\n", g_launches, g_row_plans);
   return 0;
 }

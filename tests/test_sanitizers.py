@@ -11,6 +11,7 @@
 Both are built with the system compilers (gcc / g++), never for the GPU.
 """
 import os
+import re
 import shutil
 import subprocess
 
@@ -48,3 +49,6 @@ def test_host_library_under_sanitizers(tmp_path):
           os.path.join(san, "host_check.cpp"), "-o", exe])
     r = _run([exe], env=ENV, timeout=600)
     assert "host checks ok" in r.stdout
+    # the chunk launches' row groups (every head count, n_q up to 64, spare
+    # rows) were checked by the launch stand-ins
+    assert int(re.search(r"(\d+) chunk row plans checked", r.stdout).group(1)) >= 50, r.stdout
