@@ -212,6 +212,13 @@ int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int n
   st = std::max<int64_t>(st, (lq_max + kMaxSplits - 1) / kMaxSplits);
   st = (st + gk - 1) / gk * gk;
   st = std::max<int64_t>(st, (int64_t)gk * kMinGroupsPerSplit);
+  if (nrg == 1) {
+    // Short sequences: two 32-token blocks per wave at least, while the
+    // launch still gives every compute unit a workgroup (a wave's first
+    // loads and its epilogue cost about as much as a block)
+    const int64_t two = ((int64_t)2 * 32 * kMinGroupsPerSplit + gk - 1) / gk * gk;
+    if (two > st && (total + two - 1) / two >= round / 2) st = two;
+  }
   return (int32_t)std::min<int64_t>(st, (int64_t)1 << 30);
 }
 
