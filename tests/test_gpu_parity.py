@@ -154,6 +154,25 @@ def test_split_independence_and_determinism():
         assert row_rel_err(a[0], outs[128][0].astype(np.float64)).max() <= ATTN_TOL
 
 
+@pytest.mark.parametrize("bits", [1, 2])
+def test_short_sequence_split_plan(bits):
+    # 8192 packed tokens of 8 kv heads: the plan takes two blocks per wave
+    # (256-token splits, 32 per head) instead of one; the same outputs as
+    # 128-token splits within the tolerance, and the oracle's
+    w = W(f"short8k_k{bits}", 1, 32, 8, 8192 + 37, bits, bits, R=37)
+    c = Case(w)
+    c.append_all()
+    a = c.decode()
+    kvq_set = __import__("paper_2607_16248_amd").kvq_set_split_tokens
+    kvq_set(c.cache.handle, 128)
+    b = c.decode()
+    ref = c.oracle_out(0)
+    for out in (a, b):
+        assert row_rel_err(out[0], ref).max() <= ATTN_TOL
+    log(f"[parity] {w.name}: default plan {row_rel_err(a[0], ref).max():.3e}, 128-token splits "
+        f"{row_rel_err(b[0], ref).max():.3e}")
+
+
 @pytest.mark.parametrize("L,st,n", [(4096, 128, 32), (4096, 64, 64), (4352, 32, 136), (4384, 32, 137)])
 def test_merge_at_its_load_counts(L, st, n):
     # exactly 32, 64 and 136 records per head (the largest counts one round
