@@ -164,7 +164,7 @@ chunk_mfma_kernel(DecodeArgs a) {
   // j0 + ws + kWaves*n of the split, BPG blocks each.
   const int t0 = wk.sp * a.split_tokens;
   const int t1 = min(S.Lq, t0 + a.split_tokens);
-  const int wslot = (wv + ((int)blockIdx.x >> 8)) & (kWaves - 1);
+  const int wslot = (wv + 2 * ((int)blockIdx.x >> 8)) & (kWaves - 1);
   const int j0 = t0 / a.gk + wslot, jend = t1 / a.gk;
   const int ngroups = j0 < jend ? (jend - j0 + kWaves - 1) / kWaves : 0;
   const int nblocks = ngroups * BPG;

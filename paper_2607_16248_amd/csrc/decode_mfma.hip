@@ -299,14 +299,14 @@ decode_mfma_kernel(DecodeArgs a) {
 
   // This wave's 32-token blocks: key groups j0 + ws + kWaves*n, each of
   // BPG blocks; block i is key group j0 + kWaves*(i / BPG), part i % BPG.
-  // The wave slot ws rotates with the workgroup's dispatch round (ids 256
-  // apart share a compute unit, one wave of each on every SIMD): when a
-  // split's key groups do not divide by kWaves, the extra groups go to a
-  // different SIMD in each workgroup of a compute unit instead of all to
-  // the first.
+  // The wave slot ws rotates by two with the workgroup's dispatch round
+  // (ids 256 apart share a compute unit, one wave of each on every SIMD):
+  // when a split's key groups do not divide by kWaves, the extra groups of
+  // the two workgroups of a compute unit go to different SIMDs instead of
+  // piling onto the first.
   const int t0 = wk.sp * a.split_tokens;
   const int t1 = min(S.Lq, t0 + a.split_tokens);
-  const int wslot = (wv + ((int)blockIdx.x >> 8)) & (kWaves - 1);
+  const int wslot = (wv + 2 * ((int)blockIdx.x >> 8)) & (kWaves - 1);
   const int j0 = t0 / a.gk + wslot, jend = t1 / a.gk;
   const int ngroups = j0 < jend ? (jend - j0 + kWaves - 1) / kWaves : 0;
   const int nblocks = ngroups * BPG;
