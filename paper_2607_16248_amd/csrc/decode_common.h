@@ -164,6 +164,18 @@ __device__ __forceinline__ Work find_work(const DecodeArgs& a) {
   const int ns = a.seq[si].nsplit;
   const int hv = local / ns;
   Work w{si, hv, 0, local % ns};
+  if (!CHUNK || a.nrg == 1) {
+    // the packed splits of every kv head first, the fp16-tail workgroups
+    // (split nq) after them
+    const int nq = a.seq[si].nq, packed = a.hkv * nq;
+    if (local < packed) {
+      w.h = local / nq;
+      w.sp = local - w.h * nq;
+    } else {
+      w.h = local - packed;
+      w.sp = nq;
+    }
+  }
   if (CHUNK && a.nrg > 1) {  // chunk queries: kv head and row group
     const int units = a.hkv * ns;  // (kv head, split) pairs
     if (units % 8 == 0) {

@@ -196,10 +196,13 @@ int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int n
     occ = std::min(occ, occ_rows > 0 && c->matrix[i] ? occ_rows : c->occupancy[i]);
   }
   // The fp16-tail workgroups (one per sequence and kv head with tail tokens)
-  // share the same round of resident workgroups: a workgroup that has to
-  // wait for a free slot would add a whole split's time to the launch.
+  // must not wait for a free slot (that would add a whole split's time to
+  // the launch).  Kernels that fit only two workgroups per compute unit
+  // leave them room in the round; the others take a full round of packed
+  // splits (whole blocks per wave) and the tail workgroups, which come last
+  // in id order, in their spare slots.
   const int64_t round = target_workgroups(std::min(occ, 2));
-  const int64_t target = std::max<int64_t>(round - tails, round / 2);
+  const int64_t target = occ > 2 ? round : std::max<int64_t>(round - tails, round / 2);
   int64_t st = (total + target - 1) / target;
   if (nrg > 1 && !seqs.empty()) {
     // chunk queries: every row group of a (kv head, split) unit reads the
