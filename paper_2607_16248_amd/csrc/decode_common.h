@@ -164,9 +164,9 @@ __device__ __forceinline__ Work find_work(const DecodeArgs& a) {
   const int ns = a.seq[si].nsplit;
   const int hv = local / ns;
   Work w{si, hv, 0, local % ns};
-  if (!CHUNK || a.nrg == 1) {
-    // the packed splits of every kv head first, the fp16-tail workgroups
-    // (split nq) after them
+  if (a.nqry == 1) {
+    // single-token decode: the packed splits of every kv head first, the
+    // fp16-tail workgroups (split nq, a few tokens each) after them
     const int nq = a.seq[si].nq, packed = a.hkv * nq;
     if (local < packed) {
       w.h = local / nq;

@@ -184,7 +184,7 @@ int log2_exact(int v) {
 // reads fewer records.  Fewer than two per unit (one wave per SIMD on some
 // units) measured 15-36% slower.  Classes launch one after another, so each
 // gets the whole device.
-int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int nrg, int occ_rows) {
+int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int nqry, int nrg, int occ_rows) {
   const int gk = c->d.key_group;
   if (c->split_tokens > 0) return c->split_tokens;
   int64_t total = 0, lq_max = 0, tails = 0;
@@ -197,12 +197,14 @@ int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int n
   }
   // The fp16-tail workgroups (one per sequence and kv head with tail tokens)
   // must not wait for a free slot (that would add a whole split's time to
-  // the launch).  Kernels that fit only two workgroups per compute unit
-  // leave them room in the round; the others take a full round of packed
-  // splits (whole blocks per wave) and the tail workgroups, which come last
-  // in id order, in their spare slots.
+  // the launch).  Single-token decode with kernels that fit more than two
+  // workgroups per compute unit takes a full round of packed splits (whole
+  // blocks per wave) and its tail workgroups, a few tokens each and last in
+  // id order, in spare slots; otherwise the round leaves them room (chunk
+  // queries' tail workgroups hold the queries' own tokens: started last,
+  // they would end last).
   const int64_t round = target_workgroups(std::min(occ, 2));
-  const int64_t target = occ > 2 ? round : std::max<int64_t>(round - tails, round / 2);
+  const int64_t target = nqry == 1 && occ > 2 ? round : std::max<int64_t>(round - tails, round / 2);
   int64_t st = (total + target - 1) / target;
   if (nrg > 1 && !seqs.empty()) {
     // chunk queries: every row group of a (kv head, split) unit reads the
@@ -592,7 +594,7 @@ SplitPlan plan_splits(const kvq_cache* c, int nqry = 1) {
     const int occ = nqry > 1 && matrix
                         ? kvq::matrix_decode_occupancy(cl.first.first, cl.first.second, c->d.key_group, r.rows)
                         : 0;
-    const int32_t st = split_tokens_for(c, cl.second, r.nrg, occ);
+    const int32_t st = split_tokens_for(c, cl.second, nqry, r.nrg, occ);
     for (int i : cl.second) p.st[i] = st;
   }
   p.nq.resize(B);
