@@ -168,8 +168,9 @@ __global__ __launch_bounds__(256) void decode_split_kernel(DecodeArgs a) {
 // One workgroup per (sequence, query head, 32-channel slice): thread
 // (part, c) folds the records of splits part, part + 8, ... into a running
 // (max, denominator, channel c numerator), loading U records at a time, U the
-// smallest of 4, 8 and 17 for which one memory round trip covers all splits
-// (up to 32, 64 or 136; loads past the last split would re-read it); the
+// smallest of 4, 5, 8, 9 and 17 for which one memory round trip covers all
+// splits (up to 32, 40, 64, 72 or 136: a power of two of packed splits and
+// the fp16-tail split fit; loads past the last split would re-read it); the
 // eight parts then meet in LDS.  Four slices per head spread a head's records
 // over four compute units.
 constexpr int kMergeParts = 8;
@@ -229,7 +230,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeArgs a) {
   const size_t step = (size_t)a.hq * kRecFloats;
   float M = -__builtin_inff(), D = 0.f, A = 0.f;
   if (n <= kMergeParts * 4) merge_fold<4>(base, step, n, part, c, M, D, A);
+  else if (n <= kMergeParts * 5) merge_fold<5>(base, step, n, part, c, M, D, A);
   else if (n <= kMergeParts * 8) merge_fold<8>(base, step, n, part, c, M, D, A);
+  else if (n <= kMergeParts * 9) merge_fold<9>(base, step, n, part, c, M, D, A);
   else merge_fold<17>(base, step, n, part, c, M, D, A);
   if (cs == 0) {
     sm[part] = M;

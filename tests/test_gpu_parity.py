@@ -173,10 +173,11 @@ def test_short_sequence_split_plan(bits):
         f"{row_rel_err(b[0], ref).max():.3e}")
 
 
-@pytest.mark.parametrize("L,st,n", [(4096, 128, 32), (4096, 64, 64), (4352, 32, 136), (4384, 32, 137)])
+@pytest.mark.parametrize("L,st,n", [(4096, 128, 32), (4224, 128, 33), (4096, 64, 64), (4160, 64, 65), (4608, 64, 72),
+                                     (4352, 32, 136), (4384, 32, 137)])
 def test_merge_at_its_load_counts(L, st, n):
-    # exactly 32, 64 and 136 records per head (the largest counts one round
-    # trip of 4, 8 and 17 loads per thread covers) and 137 (two rounds of 17)
+    # 32, 33, 64, 65, 72 and 136 records per head (round trips of 4, 5, 8, 9,
+    # 9 and 17 loads per thread) and 137 (two rounds of 17)
     w = W(f"merge_n{n}", 1, 32, 8, L, 1, 1)
     c = Case(w)
     c.append_all()
