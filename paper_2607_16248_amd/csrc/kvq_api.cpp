@@ -197,14 +197,17 @@ int32_t split_tokens_for(const kvq_cache* c, const std::vector<int>& seqs, int n
   }
   // The fp16-tail workgroups (one per sequence and kv head with tail tokens)
   // must not wait for a free slot (that would add a whole split's time to
-  // the launch).  Single-token decode with kernels that fit more than two
-  // workgroups per compute unit takes a full round of packed splits (whole
-  // blocks per wave) and its tail workgroups, a few tokens each and last in
-  // id order, in spare slots; otherwise the round leaves them room (chunk
-  // queries' tail workgroups hold the queries' own tokens: started last,
-  // they would end last).
+  // the launch).  Single-token decode of one sequence with kernels that fit
+  // more than two workgroups per compute unit takes a full round of packed
+  // splits (whole blocks per wave) and its tail workgroups, a few tokens
+  // each and last in id order, in spare slots; otherwise the round leaves
+  // them room (with several sequences each one's tail workgroups follow its
+  // own packed splits, so the ids past the round would be packed splits;
+  // chunk queries' tail workgroups hold the queries' own tokens: started
+  // last, they would end last).
   const int64_t round = target_workgroups(std::min(occ, 2));
-  const int64_t target = nqry == 1 && occ > 2 ? round : std::max<int64_t>(round - tails, round / 2);
+  const bool tails_spare = nqry == 1 && occ > 2 && seqs.size() == 1;
+  const int64_t target = tails_spare ? round : std::max<int64_t>(round - tails, round / 2);
   int64_t st = (total + target - 1) / target;
   if (nrg > 1 && !seqs.empty()) {
     // chunk queries: every row group of a (kv head, split) unit reads the
